@@ -1,0 +1,242 @@
+/*
+ * ema_slice.h -- C ABI of the memory-slice hot path on one MI355X (gfx950).
+ *
+ * The method is EMA's memory slice ("Elastic and Performance Transparent Memory
+ * Across GPUs"): a borrower keeps part of its paged KV cache in memory lent by
+ * a peer, prefetches it into local memory before use so remote and local
+ * blocks perform alike (local-remote symmetry, section 3), and the lender can
+ * reclaim what it lent at any time (static-dynamic symmetry, sections 3 and
+ * 4.1). Here the slice is a second, separately allocated HBM region of the
+ * same GPU standing in for the peer's share.
+ *
+ * Objects
+ *   layer-block   K and V of `block_size` consecutive tokens, all KV heads,
+ *                 one layer; 2*block_size*num_kv_heads*head_dim*2 bytes.
+ *   local pool    n_local layer-blocks; always in EMA_LAYOUT_ATTN.
+ *   slice pool    n_slice layer-blocks in the shape's slice_layout; slots at
+ *                 or above `lim` are held by the lender.
+ *   unified id    u < n_local: local block u; u >= n_local: slice slot
+ *                 u - n_local; -1: padding. Ids of different layers are
+ *                 different blocks (the pools are flat).
+ *   owner tag     >= 0: a sequence; EMA_FREE; EMA_STAGING (a local block that
+ *                 holds a prefetched copy); EMA_LENDER (slice slot at/above lim).
+ *
+ * Layouts of one layer-block (16-bit elements, K half first, then V half):
+ *   EMA_LAYOUT_ATTN  K[kv_head][token][channel], V[kv_head][channel][token]
+ *   EMA_LAYOUT_NHD   K[token][kv_head][channel], V[token][kv_head][channel]
+ *
+ * Conventions
+ *   Return value: EMA_OK or a negative EMA_ERR_*; ema_last_error() gives a
+ *   message (thread-local). Host bookkeeping is all-or-nothing: on error no
+ *   state changes.
+ *   Pointers marked "device" are HIP device pointers owned by the caller;
+ *   "host" pointers are ordinary memory. The library owns both pools.
+ *   `stream` is a hipStream_t (NULL = the null stream). Kernels are enqueued
+ *   asynchronously; host bookkeeping changes at call time. Ordering across
+ *   streams is the caller's job (events).
+ *   A handle is not thread-safe. Attention calls on one handle share its
+ *   split-K workspace: do not run two of them concurrently on different
+ *   streams.
+ *   Device paths support head_dim 128 and block_size in {16,32,64,128,256}.
+ *   Device id arrays are validated on the host only when the slice was
+ *   created with EMA_CREATE_CHECKED (it costs a device-to-host copy). Without
+ *   it, kernels skip out-of-range ids and count them; read the count with
+ *   ema_slice_device_errors().
+ */
+#ifndef EMA_SLICE_H
+#define EMA_SLICE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define EMA_OK 0
+#define EMA_ERR_INVAL (-1)   /* bad argument, range, duplicate, wrong tag  */
+#define EMA_ERR_NOMEM (-2)   /* not enough free blocks (slice: below lim)  */
+#define EMA_ERR_OWNER (-3)   /* freeing a block that is not allocated      */
+#define EMA_ERR_HIP (-4)     /* a HIP runtime call failed                  */
+
+#define EMA_F16 0
+#define EMA_BF16 1
+
+#define EMA_LAYOUT_ATTN 0
+#define EMA_LAYOUT_NHD 1
+
+#define EMA_POOL_LOCAL 0
+#define EMA_POOL_SLICE 1
+
+#define EMA_FREE (-1)
+#define EMA_STAGING (-2)
+#define EMA_LENDER (-3)
+
+#define EMA_CREATE_HOST_ONLY 1u  /* bookkeeping only: no device memory, no kernels */
+#define EMA_CREATE_CHECKED 2u    /* validate device id arrays on the host          */
+
+typedef struct ema_slice* ema_slice_t;
+
+typedef struct {
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t block_size;     /* tokens per block */
+  int32_t dtype;          /* EMA_F16 or EMA_BF16 */
+  int32_t slice_layout;   /* EMA_LAYOUT_ATTN or EMA_LAYOUT_NHD */
+} ema_kv_shape;
+
+typedef struct {
+  int64_t block_bytes;
+  int32_t n_local;
+  int32_t n_slice;
+  int32_t lim;            /* slice slots currently lent */
+  int32_t free_local;
+  int32_t free_slice;     /* FREE slots below lim */
+  int32_t device;         /* HIP device of the pools, -1 when host-only */
+  void* local_base;       /* device, library-owned, n_local*block_bytes */
+  void* slice_base;       /* device, library-owned, n_slice*block_bytes */
+} ema_slice_info;
+
+typedef struct {
+  int32_t reclaimed;      /* slots returned to the lender: min(n, lim) */
+  int32_t moved;          /* borrowed blocks copied out of the returned range */
+  int32_t written_back;   /* of those, copied into the local pool */
+  int32_t n_victims;      /* sequences preempted */
+  int32_t lim;            /* lent slots after the call */
+} ema_reclaim_result;
+
+/*
+ * slice_create -- a memory slice and the local paged cache (section 4: a slice
+ * is reserved jointly and its segments are assigned one user at a time).
+ * Allocates two separate device regions on the current HIP device:
+ * floor(local_bytes/block_bytes) local blocks and floor(lent_bytes/block_bytes)
+ * slice slots, all FREE, lim = n_slice (everything lent).
+ * flags: EMA_CREATE_HOST_ONLY (no device memory; copy and attention entry
+ * points then take host id arrays, validate them and launch nothing) and/or
+ * EMA_CREATE_CHECKED.
+ * Errors: INVAL (shape out of the supported range, NULL out), HIP (device
+ * allocation failed; nothing is leaked).
+ */
+int ema_slice_create(const ema_kv_shape* shape, size_t local_bytes, size_t lent_bytes,
+                     uint32_t flags, ema_slice_t* out);
+
+/* Frees both pools and all library scratch; synchronizes the device first. */
+int ema_slice_destroy(ema_slice_t h);
+
+/* Sizes, counts and pool base addresses. */
+int ema_slice_get_info(ema_slice_t h, ema_slice_info* out);
+
+/* Copies the owner tags: own_local[n_local], own_slice[n_slice] (host). */
+int ema_slice_owners(ema_slice_t h, int32_t* own_local, int32_t* own_slice);
+
+/*
+ * slice_alloc_blocks -- allocation first tries free memory (section 4.1).
+ * Takes the n lowest-index FREE blocks of `pool` (slice: below lim); the i-th
+ * gets owner owners[i] (>= 0, or EMA_STAGING in the local pool). Writes their
+ * unified ids to out_ids[n] (host). All or nothing.
+ * Errors: INVAL (bad pool, owner, n < 0), NOMEM (fewer than n free).
+ */
+int ema_slice_alloc_blocks(ema_slice_t h, int32_t pool, int32_t n, const int32_t* owners,
+                           int32_t* out_ids);
+
+/*
+ * Returns blocks to FREE (a finished request frees its memory, section 4.2.1).
+ * ids: host [n] unified ids. Errors: INVAL (range, duplicate), OWNER (a block
+ * that is FREE or the lender's).
+ */
+int ema_slice_free_blocks(ema_slice_t h, const int32_t* ids, int32_t n);
+
+/*
+ * The lender contributes slots again (section 6.6: an underused GPU lends its
+ * free memory): lim <- min(n_slice, lim + n_blocks); the slots become FREE.
+ * *added (host, may be NULL) receives the number added. Errors: INVAL (n < 0).
+ */
+int ema_slice_lend(ema_slice_t h, int32_t n_blocks, int32_t* added);
+
+/*
+ * slice_prefetch -- the slice process prefetches data to the accessing GPU
+ * ahead of use (section 5.1), in large transfers (section 4.2). For i < n:
+ * local block dst_block_table[i] <- slice block block_ids[i], re-laid from the
+ * slice layout into EMA_LAYOUT_ATTN. block_ids: device [n] unified ids of
+ * owned slice slots; dst_block_table: device [n] unified ids of EMA_STAGING
+ * local blocks, no duplicates. Canonical placement does not change: the
+ * destination holds a copy. Async on `stream`.
+ * Errors (checked mode or host-only): INVAL for any violation above.
+ */
+int ema_slice_prefetch(ema_slice_t h, const int32_t* block_ids, const int32_t* dst_block_table,
+                       int32_t n, void* stream);
+
+/*
+ * Moves logical blocks between pools: block dst_ids[i] <- block src_ids[i]
+ * (device [n] unified ids; each destination already allocated to the
+ * source's owner; no duplicate destinations; sources and destinations
+ * disjoint), re-laid into the destination pool's layout. The caller then
+ * frees the sources and updates its tables. Async on `stream`.
+ * Errors (checked mode or host-only): INVAL.
+ */
+int ema_slice_migrate(ema_slice_t h, const int32_t* src_ids, const int32_t* dst_ids, int32_t n,
+                      void* stream);
+
+/*
+ * slice_reclaim -- the lender takes back n_blocks lent slots (section 4.1:
+ * reclamation works on logical ownership and preempts the borrower's requests
+ * until the allocation is satisfied; a preempted request releases its local
+ * and remote blocks together, the dependency chain of section 4.1).
+ *   1. n' = min(n_blocks, lim); the top range [lim - n', lim) is returned.
+ *   2. movers: slots in that range owned by a sequence, ascending.
+ *   3. destinations: FREE slice slots below the range ascending, then FREE
+ *      local blocks ascending.
+ *   4. while movers outnumber destinations, the owner with the most movers
+ *      (ties: larger id) is preempted and every block it holds becomes FREE.
+ *   5. mover i is copied to destination i on `stream` (written-back blocks
+ *      are re-laid into EMA_LAYOUT_ATTN) and takes its owner.
+ *   6. the range becomes EMA_LENDER, lim drops by n', and every entry t of
+ *      canon_tables (device int32 [n_entries], rewritten in place on
+ *      `stream`) becomes: the destination if t was a mover, -1 if t was a
+ *      preempted sequence's block, else t.
+ * result (host, required), victims (host [victims_cap], may be NULL): the
+ * preempted owners in order; moves_src/moves_dst (host [moves_cap], may be
+ * NULL): the copies made. Counts beyond a cap are still reported in result.
+ * In host-only mode canon_tables must be NULL with n_entries 0.
+ * Errors: INVAL (n_blocks < 0, n_entries < 0, bad table pointer), HIP.
+ */
+int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, int64_t n_entries,
+                      void* stream, ema_reclaim_result* result, int32_t* victims,
+                      int32_t victims_cap, int32_t* moves_src, int32_t* moves_dst,
+                      int32_t moves_cap);
+
+/*
+ * paged_decode_attention -- one decode token per sequence over its paged KV
+ * cache in the local pool (the per-token compute whose latency must not
+ * depend on where a block started, section 6.4). For sequence b and query
+ * head hq, with kv head g = hq / (num_q_heads / num_kv_heads):
+ *   out[b][hq] = sum_t softmax_t(scale * q[b][hq] . K_t) V_t, t < seq_lens[b],
+ * token t read from row t % block_size of local block block_table[b][t / bs].
+ * q: device [batch][num_q_heads][head_dim] in the slice's dtype.
+ * block_table: device int32 [batch][max_blocks] local ids (slice ids are an
+ * error; read the prefetched staging copies instead). seq_lens: device int32
+ * [batch], each <= max_blocks*block_size; 0 gives zeros. scale <= 0 means
+ * 1/sqrt(head_dim). out: device float32 [batch][num_q_heads][head_dim].
+ * The result does not depend on which local blocks hold the tokens, bit for
+ * bit. Async on `stream`.
+ * Errors: INVAL (num_q_heads not a multiple of num_kv_heads or group > 16,
+ * batch/max_blocks < 0, unsupported shape), HIP.
+ */
+int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* block_table,
+                               const int32_t* seq_lens, int32_t batch, int32_t num_q_heads,
+                               int32_t max_blocks, float scale, float* out, void* stream);
+
+/*
+ * Synchronizes the device, then reads and clears the number of ids the
+ * kernels skipped as out of range since the last call (0 when all were valid).
+ */
+int ema_slice_device_errors(ema_slice_t h, int32_t* count);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* ema_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EMA_SLICE_H */

@@ -20,7 +20,7 @@ Operations (each all-or-nothing; on error nothing changes):
 * alloc_blocks: take the lowest-index FREE slots (slice: below lim) -- "first
   attempt to allocate from free memory" (section 4.1).
 * free_blocks / lend: give blocks back; lend raises lim (the lender contributes
-  memory again, section 6.5).
+  memory again, section 6.6).
 * prefetch: copy slice blocks into STAGING local blocks before use (section 5.1,
   the slice process prefetches ahead of access).
 * migrate: move a logical block between pools (copy to a block of the same

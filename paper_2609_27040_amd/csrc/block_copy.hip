@@ -1,0 +1,227 @@
+// Block-table-driven gather/scatter of layer-blocks between the local pool and
+// the slice (prefetch before use, migration, reclaim write-back / compaction).
+//
+// Work unit: 4 KiB of one destination block, i.e. 16 tokens x 128 channels of
+// one KV head's K or V -- one block-row at block size 16. One wavefront owns a
+// unit, four per workgroup. Same-layout units are straight 16-byte-per-lane
+// copies (each wave instruction moves 1 KiB, fully coalesced). Units that
+// change layout go through the wave's LDS tile: K rows only change order
+// (256-byte rows are re-addressed, no LDS), V is transposed between
+// [token][channel] (NHD) and [channel][token] (ATTN) in LDS so that both the
+// global reads and the global writes stay 16 bytes per lane.
+#include "kernels.h"
+
+namespace ema {
+namespace {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kUnitBytes = 4096;
+constexpr int kWaves = 4;
+constexpr int kTileRow = 128 + 8;   // u16 per LDS tile row (padded, keeps 16 B alignment)
+
+__device__ __forceinline__ u32x4 ld16(const char* p) {
+  return *reinterpret_cast<const u32x4*>(p);
+}
+__device__ __forceinline__ void st16(char* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+
+// LDS writes of this wave must land before other lanes of the wave read them.
+__device__ __forceinline__ void wave_lds_sync() {
+  __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+}
+
+__global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
+                                                         const int32_t* __restrict__ src_ids,
+                                                         const int32_t* __restrict__ dst_ids,
+                                                         int32_t n, int32_t* err_count) {
+  __shared__ __attribute__((aligned(16))) uint16_t tile[kWaves][16][kTileRow];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int upb = int(pv.block_bytes / kUnitBytes);
+  const int64_t unit = int64_t(blockIdx.x) * kWaves + wave;
+  if (unit >= int64_t(n) * upb) return;
+  const int32_t i = int32_t(unit / upb);
+  const int k = int(unit - int64_t(i) * upb);
+  const int32_t s = src_ids[i];
+  const int32_t d = dst_ids[i];
+  const int32_t n_total = pv.n_local + pv.n_slice;
+  if (s < 0 || s >= n_total || d < 0 || d >= n_total) {
+    if (k == 0 && lane == 0) atomicAdd(err_count, 1);
+    return;
+  }
+  const bool s_local = s < pv.n_local;
+  const bool d_local = d < pv.n_local;
+  const char* sb = s_local ? pv.local + int64_t(s) * pv.block_bytes
+                           : pv.slice + int64_t(s - pv.n_local) * pv.block_bytes;
+  char* db = d_local ? pv.local + int64_t(d) * pv.block_bytes
+                     : pv.slice + int64_t(d - pv.n_local) * pv.block_bytes;
+  const int s_nhd = s_local ? 0 : pv.slice_layout;
+  const int d_nhd = d_local ? 0 : pv.slice_layout;
+
+  if (s_nhd == d_nhd) {
+    const int64_t off = int64_t(k) * kUnitBytes + lane * 16;
+    const u32x4 v0 = ld16(sb + off);
+    const u32x4 v1 = ld16(sb + off + 1024);
+    const u32x4 v2 = ld16(sb + off + 2048);
+    const u32x4 v3 = ld16(sb + off + 3072);
+    st16(db + off, v0);
+    st16(db + off + 1024, v1);
+    st16(db + off + 2048, v2);
+    st16(db + off + 3072, v3);
+    return;
+  }
+
+  // Layout change. Unit k -> (half, head h, 16-token group tg).
+  const int H = pv.kv_heads;
+  const int BS = pv.block_size;
+  const int tgs = BS / 16;
+  const int uph = H * tgs;
+  const int half = k / uph;
+  const int r = k - half * uph;
+  const int h = r / tgs;
+  const int tg = r - h * tgs;
+  const int64_t half_bytes = pv.block_bytes / 2;
+
+  if (half == 0) {
+    // K: 16 rows of 256 B; ATTN row (h, t) at (h*BS + t)*256, NHD row at (t*H + h)*256.
+    u32x4 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int t = tg * 16 + j * 4 + (lane >> 4);
+      const int64_t row = s_nhd ? int64_t(t * H + h) : int64_t(h * BS + t);
+      v[j] = ld16(sb + row * 256 + (lane & 15) * 16);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int t = tg * 16 + j * 4 + (lane >> 4);
+      const int64_t row = d_nhd ? int64_t(t * H + h) : int64_t(h * BS + t);
+      st16(db + row * 256 + (lane & 15) * 16, v[j]);
+    }
+    return;
+  }
+
+  uint16_t (*T)[kTileRow] = tile[wave];
+  const char* sv = sb + half_bytes;
+  char* dv = db + half_bytes;
+  if (s_nhd) {
+    // NHD -> ATTN. Read 16 token rows (8 channels per lane) into T[t][c].
+    u32x4 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int tl = j * 4 + (lane >> 4);
+      v[j] = ld16(sv + int64_t((tg * 16 + tl) * H + h) * 256 + (lane & 15) * 16);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int tl = j * 4 + (lane >> 4);
+      *reinterpret_cast<u32x4*>(&T[tl][(lane & 15) * 8]) = v[j];
+    }
+    wave_lds_sync();
+    // Write 128 channel rows x 16 tokens: item = (c, 8-token half).
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int item = j * 64 + lane;
+      const int c = item >> 1;
+      const int t0 = (item & 1) * 8;
+      uint32_t w[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        w[q] = uint32_t(T[t0 + 2 * q][c]) | (uint32_t(T[t0 + 2 * q + 1][c]) << 16);
+      u32x4 out = {w[0], w[1], w[2], w[3]};
+      st16(dv + (int64_t(h * 128 + c) * BS + tg * 16 + t0) * 2, out);
+    }
+  } else {
+    // ATTN -> NHD. Read 128 channel rows x 16 tokens, scatter into T[t][c].
+    u32x4 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int item = j * 64 + lane;
+      const int c = item >> 1;
+      const int t0 = (item & 1) * 8;
+      v[j] = ld16(sv + (int64_t(h * 128 + c) * BS + tg * 16 + t0) * 2);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int item = j * 64 + lane;
+      const int c = item >> 1;
+      const int t0 = (item & 1) * 8;
+      const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        T[t0 + 2 * q][c] = uint16_t(w[q] & 0xffffu);
+        T[t0 + 2 * q + 1][c] = uint16_t(w[q] >> 16);
+      }
+    }
+    wave_lds_sync();
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int tl = j * 4 + (lane >> 4);
+      const u32x4 out = *reinterpret_cast<const u32x4*>(&T[tl][(lane & 15) * 8]);
+      st16(dv + int64_t((tg * 16 + tl) * H + h) * 256 + (lane & 15) * 16, out);
+    }
+  }
+}
+
+__global__ void remap_scatter_kernel(int32_t* __restrict__ remap, int32_t n_total,
+                                     const int32_t* __restrict__ keys,
+                                     const int32_t* __restrict__ vals, int32_t n) {
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int32_t key = keys[i];
+  if (key >= 0 && key < n_total) remap[key] = vals[i];
+}
+
+__global__ void iota_kernel(int32_t* __restrict__ remap, int32_t n) {
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) remap[i] = i;
+}
+
+__global__ void table_rewrite_kernel(int32_t* __restrict__ tables, int64_t n_entries,
+                                     const int32_t* __restrict__ remap, int32_t n_total) {
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; e < n_entries; e += stride) {
+    const int32_t t = tables[e];
+    if (t >= 0 && t < n_total) {
+      const int32_t nt = remap[t];
+      if (nt != t) tables[e] = nt;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32_t* dst,
+                             int32_t n, int32_t* err_count, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  const int64_t units = int64_t(n) * (pv.block_bytes / kUnitBytes);
+  const int64_t grid = (units + kWaves - 1) / kWaves;
+  hipLaunchKernelGGL(block_copy_kernel, dim3(unsigned(grid)), dim3(256), 0, stream, pv, src, dst,
+                     n, err_count);
+  return hipGetLastError();
+}
+
+hipError_t launch_remap_scatter(int32_t* remap, int32_t n_total, const int32_t* keys,
+                                const int32_t* vals, int32_t n, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(remap_scatter_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, remap,
+                     n_total, keys, vals, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_iota(int32_t* remap, int32_t n, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(iota_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, remap, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_table_rewrite(int32_t* tables, int64_t n_entries, const int32_t* remap,
+                                int32_t n_total, hipStream_t stream) {
+  if (n_entries <= 0) return hipSuccess;
+  int64_t grid = (n_entries + 255) / 256;
+  if (grid > 8192) grid = 8192;
+  hipLaunchKernelGGL(table_rewrite_kernel, dim3(unsigned(grid)), dim3(256), 0, stream, tables,
+                     n_entries, remap, n_total);
+  return hipGetLastError();
+}
+
+}  // namespace ema

@@ -1,0 +1,421 @@
+// C ABI of the memory-slice hot path (declared in include/ema_slice.h).
+//
+// One handle = host bookkeeping (SliceBook) + two separately allocated device
+// pools + library scratch: an identity remap of all unified ids used by
+// reclaim's table rewrite, a kernel error counter, an upload area for reclaim
+// copy lists (with its pinned host staging), and the attention split-K
+// workspace. Scratch grows on demand; growing synchronizes the device.
+#include "ema_slice.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "slice_book.h"
+
+struct ema_slice {
+  ema_kv_shape shape{};
+  int64_t bb = 0;
+  bool host_only = false;
+  bool checked = false;
+  int device = -1;
+  ema::SliceBook book;
+  char* local = nullptr;
+  char* slice = nullptr;
+  int32_t* d_remap = nullptr;
+  int32_t* d_err = nullptr;
+  int32_t* d_work = nullptr;
+  size_t work_cap = 0;          // ints
+  int32_t* h_work = nullptr;    // pinned
+  size_t h_work_cap = 0;        // ints
+  hipEvent_t h_work_ev = nullptr;
+  bool h_work_pending = false;
+  float* d_part = nullptr;
+  size_t part_cap = 0;          // floats
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(EMA_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define HIP_TRY(call, what)                    \
+  do {                                         \
+    hipError_t e_ = (call);                    \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+bool supported_block_size(int bs) {
+  return bs == 16 || bs == 32 || bs == 64 || bs == 128 || bs == 256;
+}
+
+ema::PoolView pool_view(const ema_slice* h) {
+  ema::PoolView pv;
+  pv.local = h->local;
+  pv.slice = h->slice;
+  pv.block_bytes = h->bb;
+  pv.n_local = h->book.n_local();
+  pv.n_slice = h->book.n_slice();
+  pv.kv_heads = h->shape.num_kv_heads;
+  pv.block_size = h->shape.block_size;
+  pv.slice_layout = h->shape.slice_layout;
+  return pv;
+}
+
+int use_device(const ema_slice* h) {
+  int cur = -1;
+  HIP_TRY(hipGetDevice(&cur), "hipGetDevice");
+  if (cur != h->device) HIP_TRY(hipSetDevice(h->device), "hipSetDevice");
+  return EMA_OK;
+}
+
+// Reads n ints of a device array to the host (checked mode).
+int fetch_ints(const int32_t* dev, int64_t n, hipStream_t st, std::vector<int32_t>* out) {
+  out->resize(size_t(n));
+  if (n == 0) return EMA_OK;
+  HIP_TRY(hipMemcpyAsync(out->data(), dev, size_t(n) * 4, hipMemcpyDeviceToHost, st),
+          "hipMemcpyAsync(check)");
+  HIP_TRY(hipStreamSynchronize(st), "hipStreamSynchronize(check)");
+  return EMA_OK;
+}
+
+int grow_device(void** p, size_t* cap, size_t need, size_t elem) {
+  if (need <= *cap) return EMA_OK;
+  HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize(grow)");
+  if (*p) HIP_TRY(hipFree(*p), "hipFree(grow)");
+  *p = nullptr;
+  *cap = 0;
+  size_t n = need + need / 4;
+  HIP_TRY(hipMalloc(p, n * elem), "hipMalloc(scratch)");
+  *cap = n;
+  return EMA_OK;
+}
+
+void release(ema_slice* h) {
+  if (!h->host_only) {
+    (void)hipDeviceSynchronize();
+    if (h->local) (void)hipFree(h->local);
+    if (h->slice) (void)hipFree(h->slice);
+    if (h->d_remap) (void)hipFree(h->d_remap);
+    if (h->d_err) (void)hipFree(h->d_err);
+    if (h->d_work) (void)hipFree(h->d_work);
+    if (h->d_part) (void)hipFree(h->d_part);
+    if (h->h_work) (void)hipHostFree(h->h_work);
+    if (h->h_work_ev) (void)hipEventDestroy(h->h_work_ev);
+  }
+  delete h;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ema_last_error(void) { return g_err.c_str(); }
+
+int ema_slice_create(const ema_kv_shape* shape, size_t local_bytes, size_t lent_bytes,
+                     uint32_t flags, ema_slice_t* out) {
+  if (!shape || !out) return fail(EMA_ERR_INVAL, "create: NULL argument");
+  *out = nullptr;
+  if (shape->num_kv_heads < 1 || shape->num_kv_heads > 64 || shape->head_dim != 128 ||
+      !supported_block_size(shape->block_size) ||
+      (shape->dtype != EMA_F16 && shape->dtype != EMA_BF16) ||
+      (shape->slice_layout != EMA_LAYOUT_ATTN && shape->slice_layout != EMA_LAYOUT_NHD))
+    return fail(EMA_ERR_INVAL, "create: unsupported shape");
+  if (flags & ~(EMA_CREATE_HOST_ONLY | EMA_CREATE_CHECKED))
+    return fail(EMA_ERR_INVAL, "create: unknown flags");
+  const int64_t bb = 2LL * shape->block_size * shape->num_kv_heads * shape->head_dim * 2;
+  const uint64_t nl = local_bytes / uint64_t(bb), ns = lent_bytes / uint64_t(bb);
+  if (nl + ns >= (1ull << 31)) return fail(EMA_ERR_INVAL, "create: more than 2^31 blocks");
+
+  ema_slice* h = new ema_slice;
+  h->shape = *shape;
+  h->bb = bb;
+  h->host_only = (flags & EMA_CREATE_HOST_ONLY) != 0;
+  h->checked = (flags & EMA_CREATE_CHECKED) != 0;
+  h->book.init(int32_t(nl), int32_t(ns));
+  if (h->host_only) {
+    *out = h;
+    return EMA_OK;
+  }
+  hipError_t e = hipGetDevice(&h->device);
+  const int32_t n_total = int32_t(nl + ns);
+  if (e == hipSuccess && nl) e = hipMalloc(&h->local, nl * bb);
+  if (e == hipSuccess && ns) e = hipMalloc(&h->slice, ns * bb);
+  if (e == hipSuccess && n_total) e = hipMalloc(&h->d_remap, size_t(n_total) * 4);
+  if (e == hipSuccess) e = hipMalloc(&h->d_err, 4);
+  if (e == hipSuccess) e = hipMemset(h->d_err, 0, 4);
+  if (e == hipSuccess) e = ema::launch_iota(h->d_remap, n_total, nullptr);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&h->h_work_ev, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    const int rc = hip_fail(e, "create");
+    release(h);
+    return rc;
+  }
+  *out = h;
+  return EMA_OK;
+}
+
+int ema_slice_destroy(ema_slice_t h) {
+  if (!h) return fail(EMA_ERR_INVAL, "destroy: NULL handle");
+  if (!h->host_only) {
+    int rc = use_device(h);
+    if (rc) return rc;
+  }
+  release(h);
+  return EMA_OK;
+}
+
+int ema_slice_get_info(ema_slice_t h, ema_slice_info* out) {
+  if (!h || !out) return fail(EMA_ERR_INVAL, "info: NULL argument");
+  out->block_bytes = h->bb;
+  out->n_local = h->book.n_local();
+  out->n_slice = h->book.n_slice();
+  out->lim = h->book.lim();
+  out->free_local = h->book.free_local();
+  out->free_slice = h->book.free_slice();
+  out->device = h->device;
+  out->local_base = h->local;
+  out->slice_base = h->slice;
+  return EMA_OK;
+}
+
+int ema_slice_owners(ema_slice_t h, int32_t* own_local, int32_t* own_slice) {
+  if (!h) return fail(EMA_ERR_INVAL, "owners: NULL handle");
+  if (own_local && h->book.n_local())
+    std::memcpy(own_local, h->book.own_local().data(), size_t(h->book.n_local()) * 4);
+  if (own_slice && h->book.n_slice())
+    std::memcpy(own_slice, h->book.own_slice().data(), size_t(h->book.n_slice()) * 4);
+  return EMA_OK;
+}
+
+int ema_slice_alloc_blocks(ema_slice_t h, int32_t pool, int32_t n, const int32_t* owners,
+                           int32_t* out_ids) {
+  if (!h) return fail(EMA_ERR_INVAL, "alloc: NULL handle");
+  std::string err;
+  const int rc = h->book.alloc(pool, n, owners, out_ids, &err);
+  return rc ? fail(rc, err) : EMA_OK;
+}
+
+int ema_slice_free_blocks(ema_slice_t h, const int32_t* ids, int32_t n) {
+  if (!h) return fail(EMA_ERR_INVAL, "free: NULL handle");
+  std::string err;
+  const int rc = h->book.free_blocks(ids, n, &err);
+  return rc ? fail(rc, err) : EMA_OK;
+}
+
+int ema_slice_lend(ema_slice_t h, int32_t n_blocks, int32_t* added) {
+  if (!h) return fail(EMA_ERR_INVAL, "lend: NULL handle");
+  std::string err;
+  const int rc = h->book.lend(n_blocks, added, &err);
+  return rc ? fail(rc, err) : EMA_OK;
+}
+
+static int copy_entry(ema_slice_t h, const int32_t* src, const int32_t* dst, int32_t n,
+                      void* stream, bool prefetch) {
+  const char* what = prefetch ? "prefetch" : "migrate";
+  if (!h) return fail(EMA_ERR_INVAL, std::string(what) + ": NULL handle");
+  if (n < 0 || (n > 0 && (!src || !dst)))
+    return fail(EMA_ERR_INVAL, std::string(what) + ": n < 0 or NULL array");
+  std::string err;
+  if (h->host_only) {
+    const int rc = prefetch ? h->book.check_prefetch(src, dst, n, &err)
+                            : h->book.check_migrate(src, dst, n, &err);
+    return rc ? fail(rc, err) : EMA_OK;
+  }
+  if (n == 0) return EMA_OK;
+  int rc = use_device(h);
+  if (rc) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (h->checked) {
+    std::vector<int32_t> hs, hd;
+    if ((rc = fetch_ints(src, n, st, &hs)) || (rc = fetch_ints(dst, n, st, &hd))) return rc;
+    rc = prefetch ? h->book.check_prefetch(hs.data(), hd.data(), n, &err)
+                  : h->book.check_migrate(hs.data(), hd.data(), n, &err);
+    if (rc) return fail(rc, err);
+  }
+  HIP_TRY(ema::launch_block_copy(pool_view(h), src, dst, n, h->d_err, st), what);
+  return EMA_OK;
+}
+
+int ema_slice_prefetch(ema_slice_t h, const int32_t* block_ids, const int32_t* dst_block_table,
+                       int32_t n, void* stream) {
+  return copy_entry(h, block_ids, dst_block_table, n, stream, true);
+}
+
+int ema_slice_migrate(ema_slice_t h, const int32_t* src_ids, const int32_t* dst_ids, int32_t n,
+                      void* stream) {
+  return copy_entry(h, src_ids, dst_ids, n, stream, false);
+}
+
+int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, int64_t n_entries,
+                      void* stream, ema_reclaim_result* result, int32_t* victims,
+                      int32_t victims_cap, int32_t* moves_src, int32_t* moves_dst,
+                      int32_t moves_cap) {
+  if (!h || !result) return fail(EMA_ERR_INVAL, "reclaim: NULL handle or result");
+  if (n_blocks < 0 || n_entries < 0 || (n_entries > 0 && !canon_tables))
+    return fail(EMA_ERR_INVAL, "reclaim: bad count or table pointer");
+  if (h->host_only && (canon_tables || n_entries))
+    return fail(EMA_ERR_INVAL, "reclaim: host-only slices take no device tables");
+  int rc;
+  if (!h->host_only && (rc = use_device(h))) return rc;
+
+  ema::ReclaimPlan plan;
+  std::string err;
+  rc = h->book.reclaim(n_blocks, &plan, &err);
+  if (rc) return fail(rc, err);
+
+  const int32_t m = int32_t(plan.move_src.size());
+  const int32_t nv = int32_t(plan.victim_blocks.size());
+  result->reclaimed = plan.reclaimed;
+  result->moved = m;
+  result->written_back = plan.written_back;
+  result->n_victims = int32_t(plan.victims.size());
+  result->lim = h->book.lim();
+  if (victims)
+    for (int32_t i = 0; i < result->n_victims && i < victims_cap; ++i) victims[i] = plan.victims[i];
+  if (moves_src && moves_dst)
+    for (int32_t i = 0; i < m && i < moves_cap; ++i) {
+      moves_src[i] = plan.move_src[i];
+      moves_dst[i] = plan.move_dst[i];
+    }
+  if (h->host_only) return EMA_OK;
+  const bool rewrite = n_entries > 0 && (m > 0 || nv > 0);
+  if (m == 0 && !rewrite) return EMA_OK;
+
+  // Upload area: keys[m+nv] | vals[m+nv] | (moves are keys[0..m) -> vals[0..m)).
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int32_t np = m + nv;
+  const size_t need = size_t(2) * np;
+  if (h->h_work_pending) {
+    HIP_TRY(hipEventSynchronize(h->h_work_ev), "hipEventSynchronize(reclaim)");
+    h->h_work_pending = false;
+  }
+  if (need > h->h_work_cap) {
+    if (h->h_work) HIP_TRY(hipHostFree(h->h_work), "hipHostFree");
+    h->h_work = nullptr;
+    h->h_work_cap = 0;
+    HIP_TRY(hipHostMalloc(&h->h_work, (need + need / 4) * 4, hipHostMallocDefault),
+            "hipHostMalloc");
+    h->h_work_cap = need + need / 4;
+  }
+  if ((rc = grow_device(reinterpret_cast<void**>(&h->d_work), &h->work_cap, need, 4))) return rc;
+  int32_t* keys = h->h_work;
+  int32_t* vals = h->h_work + np;
+  for (int32_t i = 0; i < m; ++i) {
+    keys[i] = plan.move_src[i];
+    vals[i] = plan.move_dst[i];
+  }
+  for (int32_t i = 0; i < nv; ++i) {
+    keys[m + i] = plan.victim_blocks[i];
+    vals[m + i] = -1;
+  }
+  HIP_TRY(hipMemcpyAsync(h->d_work, h->h_work, need * 4, hipMemcpyHostToDevice, st),
+          "hipMemcpyAsync(reclaim)");
+  HIP_TRY(hipEventRecord(h->h_work_ev, st), "hipEventRecord");
+  h->h_work_pending = true;
+  const int32_t* dkeys = h->d_work;
+  const int32_t* dvals = h->d_work + np;
+  const ema::PoolView pv = pool_view(h);
+  const int32_t n_total = pv.n_local + pv.n_slice;
+  HIP_TRY(ema::launch_block_copy(pv, dkeys, dvals, m, h->d_err, st), "reclaim copy");
+  if (rewrite) {
+    HIP_TRY(ema::launch_remap_scatter(h->d_remap, n_total, dkeys, dvals, np, st), "remap set");
+    HIP_TRY(ema::launch_table_rewrite(canon_tables, n_entries, h->d_remap, n_total, st),
+            "table rewrite");
+    HIP_TRY(ema::launch_remap_scatter(h->d_remap, n_total, dkeys, dkeys, np, st), "remap reset");
+  }
+  return EMA_OK;
+}
+
+int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* block_table,
+                               const int32_t* seq_lens, int32_t batch, int32_t num_q_heads,
+                               int32_t max_blocks, float scale, float* out, void* stream) {
+  if (!h) return fail(EMA_ERR_INVAL, "attention: NULL handle");
+  const int32_t hkv = h->shape.num_kv_heads;
+  if (batch < 0 || max_blocks < 0 || num_q_heads < hkv || num_q_heads % hkv != 0)
+    return fail(EMA_ERR_INVAL, "attention: bad batch, max_blocks or head counts");
+  const int32_t G = num_q_heads / hkv;
+  if (G != 1 && G != 2 && G != 4 && G != 8 && G != 16)
+    return fail(EMA_ERR_INVAL, "attention: query heads per kv head must be 1, 2, 4, 8 or 16");
+  if (batch > 65535 || hkv > 65535) return fail(EMA_ERR_INVAL, "attention: grid too large");
+  if (batch > 0 && (!q || !block_table || !seq_lens || !out))
+    return fail(EMA_ERR_INVAL, "attention: NULL array");
+  const int64_t max_tokens = int64_t(max_blocks) * h->shape.block_size;
+  if (max_tokens > (1LL << 30)) return fail(EMA_ERR_INVAL, "attention: max_blocks too large");
+  if (h->host_only || batch == 0) return EMA_OK;
+  int rc = use_device(h);
+  if (rc) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (h->checked) {
+    std::vector<int32_t> lens, tab;
+    if ((rc = fetch_ints(seq_lens, batch, st, &lens)) ||
+        (rc = fetch_ints(block_table, int64_t(batch) * max_blocks, st, &tab)))
+      return rc;
+    for (int32_t b = 0; b < batch; ++b) {
+      if (lens[b] < 0 || lens[b] > max_tokens)
+        return fail(EMA_ERR_INVAL, "attention: seq_len out of range");
+      const int32_t nb = (lens[b] + h->shape.block_size - 1) / h->shape.block_size;
+      for (int32_t j = 0; j < nb; ++j) {
+        const int32_t id = tab[size_t(b) * max_blocks + j];
+        if (id < 0 || id >= h->book.n_local())
+          return fail(EMA_ERR_INVAL, "attention: block table entry is not a local block");
+      }
+    }
+  }
+  const int32_t n_split = int32_t(std::max<int64_t>(1, (max_tokens + ema::kAttnChunk - 1) /
+                                                            ema::kAttnChunk));
+  if (n_split > 1) {
+    const size_t rows = size_t(batch) * num_q_heads * n_split;
+    if ((rc = grow_device(reinterpret_cast<void**>(&h->d_part), &h->part_cap, rows * 130, 4)))
+      return rc;
+  }
+  ema::AttnArgs a;
+  a.q = q;
+  a.table = block_table;
+  a.seq_lens = seq_lens;
+  a.out = out;
+  a.part_o = h->d_part;
+  a.part_ml = h->d_part ? h->d_part + size_t(batch) * num_q_heads * n_split * 128 : nullptr;
+  a.err_count = h->d_err;
+  a.local = h->local;
+  a.block_bytes = h->bb;
+  a.n_local = h->book.n_local();
+  a.batch = batch;
+  a.q_heads = num_q_heads;
+  a.kv_heads = hkv;
+  a.block_size = h->shape.block_size;
+  a.max_blocks = max_blocks;
+  a.n_split = n_split;
+  a.dtype = h->shape.dtype;
+  const float sc = scale > 0.0f ? scale : 1.0f / std::sqrt(float(h->shape.head_dim));
+  a.scale_log2 = sc * 1.4426950408889634f;
+  HIP_TRY(ema::launch_paged_attention(a, st), "attention launch");
+  return EMA_OK;
+}
+
+int ema_slice_device_errors(ema_slice_t h, int32_t* count) {
+  if (!h || !count) return fail(EMA_ERR_INVAL, "device_errors: NULL argument");
+  *count = 0;
+  if (h->host_only) return EMA_OK;
+  int rc = use_device(h);
+  if (rc) return rc;
+  HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize");
+  HIP_TRY(hipMemcpy(count, h->d_err, 4, hipMemcpyDeviceToHost), "hipMemcpy(err)");
+  HIP_TRY(hipMemset(h->d_err, 0, 4), "hipMemset(err)");
+  return EMA_OK;
+}
+
+}  // extern "C"

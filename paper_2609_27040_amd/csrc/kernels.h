@@ -1,0 +1,57 @@
+// Launchers of the gfx950 kernels. All take device pointers and enqueue on
+// `stream`; none allocates.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace ema {
+
+// The two pools as the kernels see them.
+struct PoolView {
+  char* local;           // n_local blocks, EMA_LAYOUT_ATTN
+  char* slice;           // n_slice blocks, slice_layout
+  int64_t block_bytes;
+  int32_t n_local;
+  int32_t n_slice;
+  int32_t kv_heads;
+  int32_t block_size;
+  int32_t slice_layout;  // 0 ATTN, 1 NHD
+};
+
+// dst[i] <- src[i] for i < n (unified ids), re-laid between pool layouts.
+// Ids outside [0, n_local + n_slice) are skipped and counted in *err_count.
+hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32_t* dst,
+                             int32_t n, int32_t* err_count, hipStream_t stream);
+
+// remap[keys[i]] = vals[i] for i < n (keys checked against n_total).
+hipError_t launch_remap_scatter(int32_t* remap, int32_t n_total, const int32_t* keys,
+                                const int32_t* vals, int32_t n, hipStream_t stream);
+
+// remap[i] = i for i < n.
+hipError_t launch_iota(int32_t* remap, int32_t n, hipStream_t stream);
+
+// t <- remap[t] for every entry 0 <= t < n_total of tables[n_entries].
+hipError_t launch_table_rewrite(int32_t* tables, int64_t n_entries, const int32_t* remap,
+                                int32_t n_total, hipStream_t stream);
+
+struct AttnArgs {
+  const void* q;            // [B][Hq][128] 16-bit
+  const int32_t* table;     // [B][max_blocks]
+  const int32_t* seq_lens;  // [B]
+  float* out;               // [B][Hq][128]
+  float* part_o;            // [B][Hq][n_split][128] split-K partial outputs
+  float* part_ml;           // [B][Hq][n_split][2] running max (log2 domain) and sum
+  int32_t* err_count;
+  const char* local;        // local pool base
+  int64_t block_bytes;
+  int32_t n_local;
+  int32_t batch, q_heads, kv_heads, block_size, max_blocks, n_split, dtype;
+  float scale_log2;         // softmax scale times log2(e)
+};
+
+constexpr int kAttnChunk = 256;   // tokens per workgroup (one split)
+
+hipError_t launch_paged_attention(const AttnArgs& a, hipStream_t stream);
+
+}  // namespace ema

@@ -1,0 +1,284 @@
+// Host bookkeeping of the memory slice: see slice_book.h.
+#include "slice_book.h"
+
+#include <algorithm>
+#include <unordered_map>
+#include <unordered_set>
+
+namespace ema {
+
+// ---------------------------------------------------------------- FreeBits --
+void FreeBits::reset(int32_t n, bool all_free) {
+  n_ = n;
+  w_.assign((size_t(n) + 63) / 64, 0ull);
+  count_ = 0;
+  if (all_free)
+    for (int32_t i = 0; i < n; ++i) set(i, true);
+}
+
+void FreeBits::set(int32_t i, bool is_free) {
+  uint64_t& w = w_[i >> 6];
+  const uint64_t bit = 1ull << (i & 63);
+  const bool was = (w & bit) != 0;
+  if (was == is_free) return;
+  if (is_free) {
+    w |= bit;
+    ++count_;
+  } else {
+    w &= ~bit;
+    --count_;
+  }
+}
+
+int32_t FreeBits::lowest(int32_t k, int32_t limit, int32_t* out) const {
+  int32_t got = 0;
+  limit = std::min(limit, n_);
+  for (size_t wi = 0; got < k && int64_t(wi) * 64 < limit; ++wi) {
+    uint64_t w = w_[wi];
+    while (w && got < k) {
+      const int32_t b = __builtin_ctzll(w);
+      const int32_t i = int32_t(wi * 64 + b);
+      if (i >= limit) return got;
+      out[got++] = i;
+      w &= w - 1;
+    }
+  }
+  return got;
+}
+
+int32_t FreeBits::count_below(int32_t limit) const {
+  limit = std::min(limit, n_);
+  int32_t c = 0;
+  const int32_t full = limit >> 6;
+  for (int32_t wi = 0; wi < full; ++wi) c += __builtin_popcountll(w_[wi]);
+  const int32_t rem = limit & 63;
+  if (rem) c += __builtin_popcountll(w_[full] & ((1ull << rem) - 1));
+  return c;
+}
+
+// --------------------------------------------------------------- SliceBook --
+void SliceBook::init(int32_t n_local, int32_t n_slice) {
+  n_local_ = n_local;
+  n_slice_ = n_slice;
+  lim_ = n_slice;
+  own_local_.assign(n_local, kFree);
+  own_slice_.assign(n_slice, kFree);
+  free_local_.reset(n_local, true);
+  free_slice_.reset(n_slice, true);
+}
+
+void SliceBook::set_owner(int32_t u, int32_t o) {
+  if (u < n_local_) {
+    own_local_[u] = o;
+    free_local_.set(u, o == kFree);
+  } else {
+    const int32_t s = u - n_local_;
+    own_slice_[s] = o;
+    free_slice_.set(s, o == kFree);
+  }
+}
+
+int SliceBook::alloc(int32_t pool, int32_t n, const int32_t* owners, int32_t* out_ids,
+                     std::string* err) {
+  if (n < 0 || (n > 0 && (!owners || !out_ids))) {
+    *err = "alloc: n < 0 or NULL array";
+    return kErrInval;
+  }
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t o = owners[i];
+    if (o < 0 && o != kStaging) {
+      *err = "alloc: bad owner " + std::to_string(o);
+      return kErrInval;
+    }
+    if (o == kStaging && pool != 0) {
+      *err = "alloc: staging blocks are local";
+      return kErrInval;
+    }
+  }
+  if (pool != 0 && pool != 1) {
+    *err = "alloc: bad pool";
+    return kErrInval;
+  }
+  FreeBits& fb = pool == 0 ? free_local_ : free_slice_;
+  const int32_t limit = pool == 0 ? n_local_ : lim_;
+  if (fb.count_below(limit) < n) {
+    *err = "alloc: not enough free blocks";
+    return kErrNomem;
+  }
+  std::vector<int32_t> slots(n);
+  const int32_t got = fb.lowest(n, limit, slots.data());
+  if (got != n) {
+    *err = "alloc: internal free-count mismatch";
+    return kErrNomem;
+  }
+  const int32_t base = pool == 0 ? 0 : n_local_;
+  for (int32_t i = 0; i < n; ++i) {
+    out_ids[i] = base + slots[i];
+    set_owner(base + slots[i], owners[i]);
+  }
+  return kOk;
+}
+
+int SliceBook::free_blocks(const int32_t* ids, int32_t n, std::string* err) {
+  if (n < 0 || (n > 0 && !ids)) {
+    *err = "free: n < 0 or NULL array";
+    return kErrInval;
+  }
+  std::unordered_set<int32_t> seen;
+  seen.reserve(size_t(n) * 2);
+  for (int32_t i = 0; i < n; ++i)
+    if (!seen.insert(ids[i]).second) {
+      *err = "free: duplicate id";
+      return kErrInval;
+    }
+  for (int32_t i = 0; i < n; ++i) {
+    if (!in_range(ids[i])) {
+      *err = "free: id out of range";
+      return kErrInval;
+    }
+    const int32_t o = owner(ids[i]);
+    if (o == kFree || o == kLender) {
+      *err = "free: block " + std::to_string(ids[i]) + " not allocated";
+      return kErrOwner;
+    }
+  }
+  for (int32_t i = 0; i < n; ++i) set_owner(ids[i], kFree);
+  return kOk;
+}
+
+int SliceBook::lend(int32_t n, int32_t* added, std::string* err) {
+  if (n < 0) {
+    *err = "lend: n < 0";
+    return kErrInval;
+  }
+  const int32_t nw = int32_t(std::min<int64_t>(n_slice_, int64_t(lim_) + n));
+  const int32_t old = lim_;
+  lim_ = nw;  // set first so the new slots count as lendable
+  for (int32_t s = old; s < nw; ++s) set_owner(n_local_ + s, kFree);
+  if (added) *added = nw - old;
+  return kOk;
+}
+
+int SliceBook::check_pairs(const int32_t* src, const int32_t* dst, int32_t n,
+                           std::string* err) const {
+  if (n < 0 || (n > 0 && (!src || !dst))) {
+    *err = "copy list: n < 0 or NULL array";
+    return kErrInval;
+  }
+  std::unordered_set<int32_t> d;
+  d.reserve(size_t(n) * 2);
+  for (int32_t i = 0; i < n; ++i)
+    if (!d.insert(dst[i]).second) {
+      *err = "copy list: duplicate destination";
+      return kErrInval;
+    }
+  for (int32_t i = 0; i < n; ++i)
+    if (d.count(src[i])) {
+      *err = "copy list: source and destination overlap";
+      return kErrInval;
+    }
+  for (int32_t i = 0; i < n; ++i)
+    if (!in_range(src[i]) || !in_range(dst[i])) {
+      *err = "copy list: id out of range";
+      return kErrInval;
+    }
+  return kOk;
+}
+
+int SliceBook::check_prefetch(const int32_t* src, const int32_t* dst, int32_t n,
+                              std::string* err) const {
+  int rc = check_pairs(src, dst, n, err);
+  if (rc) return rc;
+  for (int32_t i = 0; i < n; ++i)
+    if (src[i] < n_local_ || owner(src[i]) < 0) {
+      *err = "prefetch: source " + std::to_string(src[i]) + " is not an owned slice block";
+      return kErrInval;
+    }
+  for (int32_t i = 0; i < n; ++i)
+    if (dst[i] >= n_local_ || owner(dst[i]) != kStaging) {
+      *err = "prefetch: destination " + std::to_string(dst[i]) + " is not a staging block";
+      return kErrInval;
+    }
+  return kOk;
+}
+
+int SliceBook::check_migrate(const int32_t* src, const int32_t* dst, int32_t n,
+                             std::string* err) const {
+  int rc = check_pairs(src, dst, n, err);
+  if (rc) return rc;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t o = owner(src[i]);
+    if (o < 0 || owner(dst[i]) != o) {
+      *err = "migrate: owners differ or source unowned";
+      return kErrInval;
+    }
+  }
+  return kOk;
+}
+
+int SliceBook::reclaim(int32_t n, ReclaimPlan* p, std::string* err) {
+  if (n < 0) {
+    *err = "reclaim: n < 0";
+    return kErrInval;
+  }
+  *p = ReclaimPlan();
+  const int32_t ne = std::min(n, lim_);
+  const int32_t cut = lim_ - ne;
+  p->reclaimed = ne;
+  p->cut = cut;
+
+  std::vector<int32_t> movers;  // slice slots in [cut, lim) owned by a sequence
+  for (int32_t s = cut; s < lim_; ++s)
+    if (own_slice_[s] >= 0) movers.push_back(s);
+  auto n_dest = [&]() {
+    return int64_t(free_slice_.count_below(cut)) + free_local_.count();
+  };
+
+  while (int64_t(movers.size()) > n_dest()) {
+    std::unordered_map<int32_t, int32_t> cnt;
+    for (int32_t s : movers) ++cnt[own_slice_[s]];
+    int32_t best = -1, best_c = -1;
+    for (const auto& kv : cnt)
+      if (kv.second > best_c || (kv.second == best_c && kv.first > best)) {
+        best = kv.first;
+        best_c = kv.second;
+      }
+    p->victims.push_back(best);
+    for (int32_t u = 0; u < n_local_; ++u)
+      if (own_local_[u] == best) {
+        p->victim_blocks.push_back(u);
+        set_owner(u, kFree);
+      }
+    for (int32_t s = 0; s < n_slice_; ++s)
+      if (own_slice_[s] == best) {
+        p->victim_blocks.push_back(n_local_ + s);
+        set_owner(n_local_ + s, kFree);
+      }
+    movers.erase(std::remove_if(movers.begin(), movers.end(),
+                                [&](int32_t s) { return own_slice_[s] < 0; }),
+                 movers.end());
+  }
+
+  const int32_t m = int32_t(movers.size());
+  std::vector<int32_t> dst(m);
+  const int32_t got_s = free_slice_.lowest(m, cut, dst.data());
+  for (int32_t i = 0; i < got_s; ++i) dst[i] += n_local_;
+  const int32_t got_l = free_local_.lowest(m - got_s, n_local_, dst.data() + got_s);
+  if (got_s + got_l != m) {
+    *err = "reclaim: internal destination-count mismatch";
+    return kErrNomem;
+  }
+  p->move_src.resize(m);
+  p->move_dst = dst;
+  for (int32_t i = 0; i < m; ++i) {
+    const int32_t o = own_slice_[movers[i]];
+    p->move_src[i] = n_local_ + movers[i];
+    set_owner(dst[i], o);
+  }
+  p->written_back = got_l;
+  for (int32_t s = cut; s < lim_; ++s) set_owner(n_local_ + s, kLender);
+  lim_ = cut;
+  return kOk;
+}
+
+}  // namespace ema

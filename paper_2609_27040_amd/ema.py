@@ -1,0 +1,237 @@
+"""Thin ctypes binding of libema_slice.so -- argument marshalling only.
+
+Each function has the C entry point's name without the ``ema_`` prefix and
+passes its arguments straight through: torch tensors as their device address
+(``data_ptr()``), numpy arrays as host pointers, streams as their hipStream_t.
+Every step of the hot path runs in the library's HIP kernels; there is no
+fallback. If the library has not been built this module raises on import.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "libema_slice.so")
+
+OK, ERR_INVAL, ERR_NOMEM, ERR_OWNER, ERR_HIP = 0, -1, -2, -3, -4
+F16, BF16 = 0, 1
+LAYOUT_ATTN, LAYOUT_NHD = 0, 1
+POOL_LOCAL, POOL_SLICE = 0, 1
+FREE, STAGING, LENDER = -1, -2, -3
+CREATE_HOST_ONLY, CREATE_CHECKED = 1, 2
+DTYPES = {"f16": F16, "bf16": BF16}
+
+
+class EmaError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"ema error {code}: {msg}")
+        self.code = code
+
+
+class KVShape(ctypes.Structure):
+    _fields_ = [("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("block_size", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("slice_layout", ctypes.c_int32)]
+
+
+class SliceInfo(ctypes.Structure):
+    _fields_ = [("block_bytes", ctypes.c_int64), ("n_local", ctypes.c_int32),
+                ("n_slice", ctypes.c_int32), ("lim", ctypes.c_int32),
+                ("free_local", ctypes.c_int32), ("free_slice", ctypes.c_int32),
+                ("device", ctypes.c_int32), ("local_base", ctypes.c_void_p),
+                ("slice_base", ctypes.c_void_p)]
+
+
+class ReclaimResult(ctypes.Structure):
+    _fields_ = [("reclaimed", ctypes.c_int32), ("moved", ctypes.c_int32),
+                ("written_back", ctypes.c_int32), ("n_victims", ctypes.c_int32),
+                ("lim", ctypes.c_int32)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                          "(python -m paper_2609_27040_amd.build)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, SZ, U32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_uint32
+    sig = {
+        "ema_slice_create": [ctypes.POINTER(KVShape), SZ, SZ, U32, ctypes.POINTER(P)],
+        "ema_slice_destroy": [P],
+        "ema_slice_get_info": [P, ctypes.POINTER(SliceInfo)],
+        "ema_slice_owners": [P, P, P],
+        "ema_slice_alloc_blocks": [P, I32, I32, P, P],
+        "ema_slice_free_blocks": [P, P, I32],
+        "ema_slice_lend": [P, I32, ctypes.POINTER(I32)],
+        "ema_slice_prefetch": [P, P, P, I32, P],
+        "ema_slice_migrate": [P, P, P, I32, P],
+        "ema_slice_reclaim": [P, I32, P, I64, P, ctypes.POINTER(ReclaimResult), P, I32, P, P, I32],
+        "ema_paged_decode_attention": [P, P, P, P, I32, I32, I32, ctypes.c_float, P, P],
+        "ema_slice_device_errors": [P, ctypes.POINTER(I32)],
+    }
+    for name, args in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = ctypes.c_int
+    lib.ema_last_error.argtypes = []
+    lib.ema_last_error.restype = ctypes.c_char_p
+    return lib
+
+
+_lib = _load()
+
+
+def _check(rc):
+    if rc != OK:
+        raise EmaError(rc, _lib.ema_last_error().decode())
+
+
+def _ptr(x):
+    """Device address of a torch tensor, host address of a numpy array."""
+    if x is None:
+        return None
+    if isinstance(x, np.ndarray):
+        return x.ctypes.data
+    return x.data_ptr()
+
+
+def _i32_host(a):
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+# ---- entry points ---------------------------------------------------------------
+
+def slice_create(num_kv_heads, head_dim, block_size, dtype, slice_layout, local_bytes,
+                 lent_bytes, host_only=False, checked=False):
+    shape = KVShape(num_kv_heads, head_dim, block_size, DTYPES.get(dtype, dtype), slice_layout)
+    h = ctypes.c_void_p()
+    flags = (CREATE_HOST_ONLY if host_only else 0) | (CREATE_CHECKED if checked else 0)
+    _check(_lib.ema_slice_create(ctypes.byref(shape), int(local_bytes), int(lent_bytes), flags,
+                                 ctypes.byref(h)))
+    return h.value
+
+
+def slice_destroy(h):
+    _check(_lib.ema_slice_destroy(h))
+
+
+def slice_get_info(h):
+    info = SliceInfo()
+    _check(_lib.ema_slice_get_info(h, ctypes.byref(info)))
+    return {k: getattr(info, k) for k, _ in SliceInfo._fields_}
+
+
+def slice_owners(h):
+    info = slice_get_info(h)
+    own_l = np.empty(info["n_local"], dtype=np.int32)
+    own_s = np.empty(info["n_slice"], dtype=np.int32)
+    _check(_lib.ema_slice_owners(h, own_l.ctypes.data, own_s.ctypes.data))
+    return own_l, own_s, info["lim"]
+
+
+def slice_alloc_blocks(h, pool, owners):
+    owners = _i32_host(owners)
+    out = np.empty(len(owners), dtype=np.int32)
+    _check(_lib.ema_slice_alloc_blocks(h, pool, len(owners), owners.ctypes.data, out.ctypes.data))
+    return out
+
+
+def slice_free_blocks(h, ids):
+    ids = _i32_host(ids)
+    _check(_lib.ema_slice_free_blocks(h, ids.ctypes.data, len(ids)))
+
+
+def slice_lend(h, n_blocks):
+    added = ctypes.c_int32()
+    _check(_lib.ema_slice_lend(h, int(n_blocks), ctypes.byref(added)))
+    return added.value
+
+
+def slice_prefetch(h, block_ids, dst_block_table, n=None, stream=None):
+    """block_ids, dst_block_table: int32 device tensors (numpy arrays for a
+    host-only slice)."""
+    n = len(block_ids) if n is None else n
+    host = isinstance(block_ids, np.ndarray)
+    if host:
+        block_ids, dst_block_table = _i32_host(block_ids), _i32_host(dst_block_table)
+    _check(_lib.ema_slice_prefetch(h, _ptr(block_ids), _ptr(dst_block_table), int(n),
+                                   None if host else _stream(stream)))
+
+
+def slice_migrate(h, src_ids, dst_ids, n=None, stream=None):
+    n = len(src_ids) if n is None else n
+    host = isinstance(src_ids, np.ndarray)
+    if host:
+        src_ids, dst_ids = _i32_host(src_ids), _i32_host(dst_ids)
+    _check(_lib.ema_slice_migrate(h, _ptr(src_ids), _ptr(dst_ids), int(n),
+                                  None if host else _stream(stream)))
+
+
+def slice_reclaim(h, n_blocks, canon_tables=None, stream=None, caps=None):
+    """canon_tables: int32 device tensor rewritten in place (None for none).
+    Returns the result counts plus the victims and the copies made."""
+    info = slice_get_info(h)
+    cap = int(caps) if caps is not None else info["n_local"] + info["n_slice"]
+    res = ReclaimResult()
+    victims = np.empty(max(cap, 1), dtype=np.int32)
+    msrc = np.empty(max(cap, 1), dtype=np.int32)
+    mdst = np.empty(max(cap, 1), dtype=np.int32)
+    n_entries = 0 if canon_tables is None else canon_tables.numel()
+    host_only = info["device"] < 0
+    _check(_lib.ema_slice_reclaim(h, int(n_blocks), _ptr(canon_tables), n_entries,
+                                  None if host_only else _stream(stream), ctypes.byref(res),
+                                  victims.ctypes.data, cap, msrc.ctypes.data, mdst.ctypes.data,
+                                  cap))
+    m = min(res.moved, cap)
+    return {"reclaimed": res.reclaimed, "moved": res.moved, "written_back": res.written_back,
+            "victims": victims[:min(res.n_victims, cap)].tolist(), "lim": res.lim,
+            "moves": list(zip(msrc[:m].tolist(), mdst[:m].tolist()))}
+
+
+def paged_decode_attention(h, q, block_table, seq_lens, out, scale=0.0, stream=None):
+    """q [B][Hq][D] (16-bit), block_table int32 [B][max_blocks], seq_lens int32
+    [B], out float32 [B][Hq][D]: device tensors."""
+    B, Hq = int(q.shape[0]), int(q.shape[1])
+    max_blocks = int(block_table.shape[1]) if block_table.dim() == 2 else 0
+    _check(_lib.ema_paged_decode_attention(h, _ptr(q), _ptr(block_table), _ptr(seq_lens), B, Hq,
+                                           max_blocks, float(scale), _ptr(out), _stream(stream)))
+
+
+def slice_device_errors(h):
+    c = ctypes.c_int32()
+    _check(_lib.ema_slice_device_errors(h, ctypes.byref(c)))
+    return c.value
+
+
+# ---- plumbing: library-owned pools as torch tensors ---------------------------------
+
+class _DeviceBuffer:
+    def __init__(self, ptr, nbytes):
+        self.__cuda_array_interface__ = {"shape": (int(nbytes),), "typestr": "|u1",
+                                         "data": (int(ptr), False), "version": 3,
+                                         "strides": None}
+
+
+def pool_view(h, pool):
+    """uint8 torch tensor [n_blocks][block_bytes] aliasing a library pool.
+    Valid until slice_destroy(h)."""
+    import torch
+    info = slice_get_info(h)
+    n = info["n_local"] if pool == POOL_LOCAL else info["n_slice"]
+    base = info["local_base"] if pool == POOL_LOCAL else info["slice_base"]
+    if n == 0 or not base:
+        return torch.empty((0, info["block_bytes"]), dtype=torch.uint8, device="cuda")
+    t = torch.as_tensor(_DeviceBuffer(base, n * info["block_bytes"]), device="cuda")
+    return t.view(n, info["block_bytes"])
+
+
+def last_error():
+    return _lib.ema_last_error().decode()

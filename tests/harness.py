@@ -1,0 +1,189 @@
+"""Sets a synthetic KV-cache workload up in the library (GPU tests and bench).
+
+A ``Workload`` owns one slice handle sized for the config: every logical
+block of every layer allocated (local or slice per the seeded placement, in a
+seeded random order so physical ids are scattered), ``staging_slots`` layers'
+worth of STAGING local blocks as the prefetch double buffer, and device copies
+of the canonical tables, per-layer prefetch lists and per-layer attention
+tables (canonical with each slice id replaced by the staging block it is
+prefetched into).
+
+Values: ``fill="host"`` draws every pool element on the host (iid N(0,1)
+rounded to 16 bits) and writes NaN into unused tail token slots, keeping a host
+image for the oracle; ``fill="device"`` draws them on the GPU with a seeded
+torch generator (large configs) and the oracle reads back what it needs.
+"""
+import numpy as np
+import torch
+
+import synth
+from paper_2609_27040_amd import ema
+
+TORCH_DT = {"f16": torch.float16, "bf16": torch.bfloat16}
+
+
+class Workload:
+    def __init__(self, cfg, layers=None, batch=None, slice_layout=ema.LAYOUT_ATTN, seed=None,
+                 staging_slots=2, extra_local=0, extra_slice=0, fill="host", checked=False,
+                 lens=None, frac=None):
+        self.cfg = cfg = cfg if batch is None else cfg.scaled(batch=batch)
+        self.L = cfg.layers if layers is None else layers
+        rng = np.random.default_rng(cfg.seed if seed is None else seed)
+        self.lens = synth.seq_lens(cfg, rng) if lens is None else np.asarray(lens, np.int64)
+        self.B = len(self.lens)
+        self.pl = pl = synth.placement(cfg, self.lens, rng, frac=frac, layers=self.L)
+        self.bs, self.hkv, self.D = cfg.block_size, cfg.kv_heads, cfg.head_dim
+        self.bb = cfg.block_bytes
+        self.maxblk = max(pl.maxblk, 1)
+        self.slice_layout = slice_layout
+        self.slice_per_layer = pl.in_slice.reshape(self.L, -1).sum(axis=1)
+        self.stage_n = int(self.slice_per_layer.max()) if self.L else 0
+        self.staging_slots = staging_slots
+        n_local = len(pl.local_order) + staging_slots * self.stage_n + extra_local
+        n_slice = len(pl.slice_order) + extra_slice
+        self.h = ema.slice_create(self.hkv, self.D, self.bs, cfg.dtype, slice_layout,
+                                  n_local * self.bb, n_slice * self.bb, checked=checked)
+        self.alloc_log = []
+        tables = np.full((self.L, self.B, self.maxblk), -1, dtype=np.int64)
+        for pool, order in ((ema.POOL_LOCAL, pl.local_order), (ema.POOL_SLICE, pl.slice_order)):
+            if len(order):
+                owners = order[:, 1]
+                ids = ema.slice_alloc_blocks(self.h, pool, owners)
+                self.alloc_log.append((pool, owners.copy()))
+                tables[order[:, 0], order[:, 1], order[:, 2]] = ids
+        self.tables = tables
+        st_owners = np.full(staging_slots * self.stage_n, ema.STAGING)
+        self.staging = ema.slice_alloc_blocks(self.h, ema.POOL_LOCAL, st_owners).reshape(
+            staging_slots, self.stage_n) if len(st_owners) else np.zeros((staging_slots, 0), np.int32)
+        self.alloc_log.append((ema.POOL_LOCAL, st_owners))
+        info = ema.slice_get_info(self.h)
+        self.n_local = info["n_local"]
+        # per-layer prefetch lists and attention tables
+        self.pf_src, self.pf_dst = [], []
+        attn = tables.copy()
+        for l in range(self.L):
+            mask = tables[l] >= self.n_local
+            src = tables[l][mask]
+            dst = self.staging[l % staging_slots, :len(src)]
+            attn[l][mask] = dst
+            self.pf_src.append(src.astype(np.int32))
+            self.pf_dst.append(dst.astype(np.int32))
+        self.attn_tables = attn
+        self.q16 = synth.q_values(cfg, rng, self.B)
+        dev = torch.device("cuda")
+        self.q = torch.from_numpy(self.q16.view(np.int16)).to(dev).view(TORCH_DT[cfg.dtype])
+        self.lens_dev = torch.from_numpy(self.lens.astype(np.int32)).to(dev)
+        self.tables_dev = torch.from_numpy(tables.astype(np.int32)).to(dev)
+        self.attn_dev = torch.from_numpy(attn.astype(np.int32)).to(dev)
+        self.pf_src_dev = [torch.from_numpy(s).to(dev) for s in self.pf_src]
+        self.pf_dst_dev = [torch.from_numpy(d).to(dev) for d in self.pf_dst]
+        self.local_view = ema.pool_view(self.h, ema.POOL_LOCAL)
+        self.slice_view = ema.pool_view(self.h, ema.POOL_SLICE)
+        self.host_local = self.host_slice = None
+        if fill == "host":
+            self._fill_host(rng)
+        elif fill == "device":
+            self._fill_device(cfg.seed if seed is None else seed)
+        torch.cuda.synchronize()
+
+    # ---- values -----------------------------------------------------------------
+    def _tail_positions(self, layout):
+        """(block-row index into tables, element indices) of unused tail slots."""
+        out = []
+        for b in range(self.B):
+            n = int(self.lens[b])
+            r = n % self.bs
+            if n == 0 or r == 0:
+                continue
+            j = (n - 1) // self.bs
+            t = np.arange(r, self.bs)
+            h, tt, d = np.meshgrid(np.arange(self.hkv), t, np.arange(self.D), indexing="ij")
+            idx = np.concatenate([synth.element_index(layout, half, h, tt, d, self.hkv, self.bs,
+                                                      self.D).ravel() for half in (0, 1)])
+            out.append((b, j, idx))
+        return out
+
+    def _fill_host(self, rng):
+        n_l, n_s = self.local_view.shape[0], self.slice_view.shape[0]
+        half = self.bb // 2
+        loc = synth.random_16bit(rng, (n_l, half), self.cfg.dtype)
+        sli = synth.random_16bit(rng, (n_s, half), self.cfg.dtype)
+        nan = synth.NAN16[self.cfg.dtype]
+        for pool_arr, layout, is_slice in ((loc, synth.LAYOUT_ATTN, False),
+                                           (sli, self.slice_layout, True)):
+            for b, j, idx in self._tail_positions(layout):
+                for l in range(self.L):
+                    u = int(self.tables[l, b, j])
+                    if (u >= self.n_local) == is_slice:
+                        pool_arr[u - self.n_local if is_slice else u, idx] = nan
+        # staging blocks start as a recognisable sentinel
+        stg = self.staging.ravel()
+        loc[stg] = 0xA5A5
+        self.host_local = loc.view(np.uint8).reshape(n_l, self.bb)
+        self.host_slice = sli.view(np.uint8).reshape(n_s, self.bb)
+        self.local_view.copy_(torch.from_numpy(self.host_local))
+        if n_s:
+            self.slice_view.copy_(torch.from_numpy(self.host_slice))
+
+    def _fill_device(self, seed):
+        g = torch.Generator(device="cuda")
+        g.manual_seed(int(seed))
+        dt = TORCH_DT[self.cfg.dtype]
+        for view in (self.local_view, self.slice_view):
+            flat = view.view(-1).view(dt)
+            chunk = 1 << 28
+            for s in range(0, flat.numel(), chunk):
+                e = min(flat.numel(), s + chunk)
+                flat[s:e].copy_(torch.randn(e - s, generator=g, device="cuda", dtype=torch.float32))
+
+    # ---- the hot path ---------------------------------------------------------------
+    def prefetch(self, l, stream=None):
+        ema.slice_prefetch(self.h, self.pf_src_dev[l], self.pf_dst_dev[l], len(self.pf_src[l]),
+                           stream=stream)
+
+    def attention(self, l, out, table=None, stream=None):
+        ema.paged_decode_attention(self.h, self.q, self.attn_dev[l] if table is None else table,
+                                   self.lens_dev, out, stream=stream)
+
+    def new_out(self):
+        return torch.empty((self.B, self.cfg.q_heads, self.D), dtype=torch.float32, device="cuda")
+
+    def close(self):
+        self.local_view = self.slice_view = None
+        torch.cuda.synchronize()
+        ema.slice_destroy(self.h)
+
+    # ---- oracle side ------------------------------------------------------------------
+    def oracle_mirror(self):
+        """An oracle slice replaying the same allocations, holding the host image."""
+        import oracle
+        st = oracle.SliceOracle(self.hkv, self.D, self.bs, self.cfg.dtype, self.slice_layout,
+                                self.local_view.shape[0] * self.bb,
+                                self.slice_view.shape[0] * self.bb)
+        for pool, owners in self.alloc_log:
+            st.alloc_blocks(pool, owners)
+        own_l, own_s, lim = ema.slice_owners(self.h)
+        assert np.array_equal(own_l, st.own_local) and np.array_equal(own_s, st.own_slice)
+        st.local[:] = self.host_local
+        st.slice[:] = self.host_slice
+        return st
+
+
+def rel_err(out, ref):
+    """max over (b, h) of ||o - ref||_inf / ||ref||_inf (rows with ref == 0: absolute)."""
+    out = np.asarray(out, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    num = np.abs(out - ref).max(axis=-1)
+    den = np.abs(ref).max(axis=-1)
+    den = np.where(den > 0, den, 1.0)
+    return float((num / den).max()) if num.size else 0.0
+
+
+def read_blocks(view, ids):
+    """Host copies of the given blocks of a pool view (id -> bytes)."""
+    ids = np.unique(np.asarray(ids, dtype=np.int64))
+    ids = ids[ids >= 0]
+    if not len(ids):
+        return {}
+    data = view[torch.from_numpy(ids).to(view.device)].cpu().numpy()
+    return {int(u): data[i] for i, u in enumerate(ids)}

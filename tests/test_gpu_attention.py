@@ -1,0 +1,178 @@
+"""GPU parity of paged decode attention against the float64 oracle.
+
+Bar: max over (sequence, query head) of ||o - ref||_inf / ||ref||_inf <= 2e-3
+(16-bit inputs, fp32 accumulation and fp32 output). Unused tail token slots
+hold NaN so masking is exercised; staging blocks start as a sentinel.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from harness import Workload, rel_err, read_blocks
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-3
+
+
+@pytest.fixture(scope="module")
+def ema():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_27040_amd import ema as m
+    return m
+
+
+def oracle_attention(w, st, l):
+    return oracle.paged_decode_attention(w.q16, w.attn_tables[l], w.lens, st.read_block, w.hkv,
+                                         w.D, w.bs, w.cfg.dtype)
+
+
+@pytest.mark.parametrize("layout", [0, 1])
+def test_tiny_config_end_to_end(ema, layout):
+    """The tiny workload in full: prefetch the slice half into staging, decode
+    one token per sequence, then reclaim every lent block."""
+    print(f"tiny layout={layout}", flush=True)
+    w = Workload(synth.TINY, slice_layout=layout, staging_slots=1, extra_local=200)
+    try:
+        st = w.oracle_mirror()
+        w.prefetch(0)
+        st.prefetch(w.pf_src[0], w.pf_dst[0])
+        out = w.new_out()
+        w.attention(0, out)
+        torch.cuda.synchronize()
+        assert ema.slice_device_errors(w.h) == 0
+        got = out.cpu().numpy()
+        assert np.all(np.isfinite(got))
+        ref = oracle_attention(w, st, 0)
+        assert rel_err(got, ref) <= TOL
+        assert np.array_equal(w.local_view.cpu().numpy(), st.local)     # prefetch bit-exact
+        # reclaim everything lent; tables rewritten on the device
+        r = ema.slice_reclaim(w.h, 10 ** 9, w.tables_dev.view(-1))
+        ro = st.reclaim(10 ** 9, w.tables)
+        assert r["moves"] == ro["moves"] and r["victims"] == ro["victims"]
+        assert r["lim"] == 0 and ro["lim"] == 0
+        assert np.array_equal(w.tables_dev.cpu().numpy(), w.tables)
+        torch.cuda.synchronize()
+        assert np.array_equal(w.local_view.cpu().numpy(), st.local)
+        oracle.check_sd_symmetry(st)
+        oracle.check_ownership(st, w.tables)
+    finally:
+        w.close()
+
+
+SHAPES = [  # (q_heads, kv_heads, block_size, dtype)
+    (8, 8, 16, "f16"), (32, 8, 16, "bf16"), (8, 1, 32, "bf16"), (4, 2, 64, "f16"),
+    (16, 1, 16, "bf16"), (2, 2, 256, "f16"), (16, 4, 128, "bf16"),
+]
+LENS = [0, 1, 15, 16, 17, 255, 256, 257, 511, 513, 1000, 2049]
+
+
+@pytest.mark.parametrize("hq,hkv,bs,dtype", SHAPES)
+def test_attention_shapes_and_ragged_lengths(ema, hq, hkv, bs, dtype):
+    print(f"attn hq={hq} hkv={hkv} bs={bs} {dtype}", flush=True)
+    cfg = synth.KVConfig("grid", 1, hq, hkv, 128, dtype, bs, len(LENS), ("uniform", 0, 0), 0.4,
+                         31 + bs)
+    w = Workload(cfg, lens=LENS, staging_slots=1)
+    try:
+        st = w.oracle_mirror()
+        w.prefetch(0)
+        st.prefetch(w.pf_src[0], w.pf_dst[0])
+        out = w.new_out()
+        w.attention(0, out)
+        torch.cuda.synchronize()
+        assert ema.slice_device_errors(w.h) == 0
+        got = out.cpu().numpy()
+        ref = oracle_attention(w, st, 0)
+        assert np.all(got[0] == 0.0)                    # empty sequence
+        assert rel_err(got, ref) <= TOL, rel_err(got, ref)
+    finally:
+        w.close()
+
+
+def test_staged_and_all_local_tables_give_identical_bits(ema):
+    """Local-remote symmetry as a functional property: the same tokens read
+    from staging copies or from other local blocks give the same bits."""
+    cfg = synth.LLAMA8B.scaled(layers=1, batch=6)
+    w = Workload(cfg, staging_slots=1, extra_local=4000, fill="device")
+    try:
+        w.prefetch(0)
+        out_a = w.new_out()
+        w.attention(0, out_a)
+        # copy every block of layer 0 to fresh local blocks of the same owner
+        tab = w.tables[0]
+        valid = tab >= 0
+        owners = np.nonzero(valid)[0]
+        fresh = ema.slice_alloc_blocks(w.h, ema.POOL_LOCAL, owners)
+        src = torch.as_tensor(tab[valid].astype(np.int32), device="cuda")
+        dst = torch.as_tensor(fresh, device="cuda")
+        ema.slice_migrate(w.h, src, dst)
+        tab2 = np.full_like(tab, -1)
+        tab2[valid] = fresh
+        out_b = w.new_out()
+        w.attention(0, out_b, table=torch.as_tensor(tab2.astype(np.int32), device="cuda"))
+        torch.cuda.synchronize()
+        assert ema.slice_device_errors(w.h) == 0
+        assert torch.equal(out_a, out_b)
+    finally:
+        w.close()
+
+
+def test_checked_mode_rejects_slice_ids_in_attention_table(ema):
+    cfg = synth.TINY.scaled(batch=2)
+    w = Workload(cfg, staging_slots=1, checked=True)
+    try:
+        out = w.new_out()
+        with pytest.raises(ema.EmaError) as e:
+            w.attention(0, out, table=w.tables_dev[0])  # canonical table still has slice ids
+        assert e.value.code == ema.ERR_INVAL
+    finally:
+        w.close()
+
+
+def sampled_parity(ema, w, layer, samples, rng):
+    w.prefetch(layer)
+    out = w.new_out()
+    w.attention(layer, out)
+    torch.cuda.synchronize()
+    assert ema.slice_device_errors(w.h) == 0
+    got = out.cpu().numpy()
+    bs = w.bs
+    pick = rng.choice(w.B, size=min(samples, w.B), replace=False)
+    for b in pick:
+        nb = (int(w.lens[b]) + bs - 1) // bs
+        ids = w.attn_tables[layer, b, :nb]
+        blocks = read_blocks(w.local_view, ids)
+        ref = oracle.paged_decode_attention(w.q16[b:b + 1], w.attn_tables[layer, b:b + 1],
+                                            w.lens[b:b + 1], blocks.__getitem__, w.hkv, w.D, bs,
+                                            w.cfg.dtype)
+        assert rel_err(got[b:b + 1], ref) <= TOL, (b, rel_err(got[b:b + 1], ref))
+        # the staged copies are the slice blocks, bit for bit
+        canon = w.tables[layer, b, :nb]
+        sl = canon >= w.n_local
+        if sl.any():
+            src = read_blocks(w.slice_view, canon[sl] - w.n_local)
+            for u, s in zip(ids[sl], canon[sl] - w.n_local):
+                if w.slice_layout == 0:
+                    assert np.array_equal(blocks[int(u)], src[int(s)])
+    return got
+
+
+def test_llama8b_shaped_layer_sampled(ema):
+    print("llama8b layer", flush=True)
+    w = Workload(synth.LLAMA8B, layers=2, fill="device")
+    try:
+        sampled_parity(ema, w, 1, 6, np.random.default_rng(1))
+    finally:
+        w.close()
+
+
+def test_70b_tp8_share_layer_sampled(ema):
+    print("70b share layer", flush=True)
+    w = Workload(synth.L70B_TP8, layers=2, fill="device")
+    try:
+        assert w.lens.max() > 4096                      # long tails exercise many splits
+        sampled_parity(ema, w, 0, 6, np.random.default_rng(2))
+    finally:
+        w.close()

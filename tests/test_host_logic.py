@@ -1,0 +1,130 @@
+"""Host bookkeeping of the C-ABI library against the oracle, on the CPU.
+
+The library is created host-only (no device memory): allocation, freeing,
+lending, copy-list validation and the reclaim planner are the same C++ code
+the GPU path runs. Random traces drive the library and the oracle side by side;
+ids, error codes, owner tags, lent limit, reclaim plans and rewritten tables
+must match exactly after every operation.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from trace import Cache, OracleBackend, random_trace
+
+LIB = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                   "paper_2609_27040_amd", "lib", "libema_slice.so")
+pytestmark = pytest.mark.skipif(not os.path.exists(LIB), reason="library not built")
+
+HKV, D, BS = 2, 128, 16
+BB = 2 * BS * HKV * D * 2
+
+
+class LibHostBackend:
+    """The library in host-only mode. Table rewriting is the device's job, so
+    this adapter applies the returned plan to host tables itself."""
+
+    def __init__(self, n_local, n_slice, layout=0):
+        from paper_2609_27040_amd import ema
+        self.ema = ema
+        self.h = ema.slice_create(HKV, D, BS, "f16", layout, n_local * BB, n_slice * BB,
+                                  host_only=True)
+        self.n_local = n_local
+
+    def close(self):
+        self.ema.slice_destroy(self.h)
+
+    def alloc_blocks(self, where, owners):
+        return self.ema.slice_alloc_blocks(self.h, where, owners).astype(np.int64)
+
+    def free_blocks(self, ids):
+        self.ema.slice_free_blocks(self.h, ids)
+
+    def lend(self, n):
+        return self.ema.slice_lend(self.h, n)
+
+    def migrate(self, src, dst):
+        self.ema.slice_migrate(self.h, np.asarray(src), np.asarray(dst))
+
+    def prefetch(self, src, dst):
+        self.ema.slice_prefetch(self.h, np.asarray(src), np.asarray(dst))
+
+    def reclaim(self, n, tables):
+        own_l, own_s, _ = self.ema.slice_owners(self.h)
+        owners_before = np.concatenate([own_l, own_s])
+        r = self.ema.slice_reclaim(self.h, n)
+        remap = {s: d for s, d in r["moves"]}
+        victims = set(r["victims"])
+        flat = tables.reshape(-1)
+        for i, t in enumerate(flat):
+            if t < 0:
+                continue
+            if int(owners_before[t]) in victims:
+                flat[i] = -1
+            elif int(t) in remap:
+                flat[i] = remap[int(t)]
+        return {k: r[k] for k in ("reclaimed", "moved", "written_back", "victims", "lim",
+                                  "moves")}
+
+    def owners(self):
+        return self.ema.slice_owners(self.h)
+
+
+def compare_owners(st, lib):
+    own_l, own_s, lim = lib.owners()
+    assert np.array_equal(own_l, st.own_local) and np.array_equal(own_s, st.own_slice)
+    assert lim == st.lim
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_library_bookkeeping_matches_oracle_on_random_traces(seed):
+    rng = np.random.default_rng(1000 + seed)
+    n_local, n_slice = int(rng.integers(6, 30)), int(rng.integers(4, 24))
+    st = oracle.SliceOracle(HKV, D, BS, "f16", 0, n_local * BB, n_slice * BB, with_data=False)
+    lib = LibHostBackend(n_local, n_slice)
+    try:
+        cache = Cache([OracleBackend(st), lib], layers=3, batch=6, maxblk=5, rng=rng)
+        random_trace(cache, 300, rng, on_step=lambda step, op: compare_owners(st, lib))
+        cache.reclaim(int(rng.integers(0, n_slice + 3)))
+        compare_owners(st, lib)
+    finally:
+        lib.close()
+
+
+def test_error_codes_match_the_oracle():
+    st = oracle.SliceOracle(HKV, D, BS, "f16", 0, 4 * BB, 4 * BB, with_data=False)
+    lib = LibHostBackend(4, 4)
+    try:
+        cache = Cache([OracleBackend(st), lib], layers=1, batch=2, maxblk=4,
+                      rng=np.random.default_rng(0))
+        cases = [("alloc_blocks", 0, [0] * 5), ("alloc_blocks", 1, [-2]), ("alloc_blocks", 3, [0]),
+                 ("alloc_blocks", 0, [-7]), ("free_blocks", [0]), ("free_blocks", [99]),
+                 ("lend", -1), ("migrate", [0], [1]), ("prefetch", [4], [0])]
+        for name, *args in cases:
+            _, err = cache._all(name, *args)
+            assert err is not None, (name, args)
+    finally:
+        lib.close()
+
+
+def test_large_pool_reclaim_plan_matches_oracle():
+    """A big, fragmented slice: one reclaim of most of the lent range."""
+    rng = np.random.default_rng(7)
+    n_local, n_slice = 400, 600
+    st = oracle.SliceOracle(HKV, D, BS, "f16", 0, n_local * BB, n_slice * BB, with_data=False)
+    lib = LibHostBackend(n_local, n_slice)
+    try:
+        cache = Cache([OracleBackend(st), lib], layers=2, batch=40, maxblk=12, rng=rng)
+        for _ in range(300):
+            cache.grow(int(rng.integers(2)), int(rng.integers(40)), int(rng.integers(2)),
+                       int(rng.integers(1, 6)))
+        for b in rng.choice(40, 8, replace=False):
+            cache.finish(int(b))
+        r = cache.reclaim(450)
+        assert r["moved"] > 0
+        compare_owners(st, lib)
+        oracle.check_ownership(st, cache.tables)
+    finally:
+        lib.close()
