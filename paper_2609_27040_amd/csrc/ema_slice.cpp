@@ -10,6 +10,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -36,6 +37,7 @@ struct ema_slice {
   bool h_work_pending = false;
   float* d_part = nullptr;
   size_t part_cap = 0;          // floats
+  bool attn_valu = false;         // EMA_ATTN_KERNEL=valu selects the vector-ALU kernel
 };
 
 namespace {
@@ -144,6 +146,8 @@ int ema_slice_create(const ema_kv_shape* shape, size_t local_bytes, size_t lent_
   h->bb = bb;
   h->host_only = (flags & EMA_CREATE_HOST_ONLY) != 0;
   h->checked = (flags & EMA_CREATE_CHECKED) != 0;
+  const char* impl = std::getenv("EMA_ATTN_KERNEL");
+  h->attn_valu = impl && std::strcmp(impl, "valu") == 0;
   h->book.init(int32_t(nl), int32_t(ns));
   if (h->host_only) {
     *out = h;
@@ -375,8 +379,13 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
       }
     }
   }
-  const int32_t n_split = int32_t(std::max<int64_t>(1, (max_tokens + ema::kAttnChunk - 1) /
-                                                            ema::kAttnChunk));
+  // Tokens per workgroup: the vector-ALU kernel uses a fixed chunk; the
+  // matrix-core kernel takes 512-token chunks when there are enough
+  // (sequence, KV head) pairs to fill the GPU, else 256 for more splits.
+  const int32_t chunk = h->attn_valu ? ema::kAttnChunk
+                                     : (int64_t(batch) * hkv >= 256 ? 512 : 256);
+  const int32_t n_split = int32_t(std::max<int64_t>(1, (max_tokens + chunk - 1) / chunk));
+  if (n_split > 65535) return fail(EMA_ERR_INVAL, "attention: max_blocks too large");
   if (n_split > 1) {
     const size_t rows = size_t(batch) * num_q_heads * n_split;
     if ((rc = grow_device(reinterpret_cast<void**>(&h->d_part), &h->part_cap, rows * 130, 4)))
@@ -400,9 +409,12 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
   a.max_blocks = max_blocks;
   a.n_split = n_split;
   a.dtype = h->shape.dtype;
+  a.chunk = chunk;
   const float sc = scale > 0.0f ? scale : 1.0f / std::sqrt(float(h->shape.head_dim));
   a.scale_log2 = sc * 1.4426950408889634f;
-  HIP_TRY(ema::launch_paged_attention(a, st), "attention launch");
+  HIP_TRY(h->attn_valu ? ema::launch_paged_attention(a, st)
+                       : ema::launch_paged_attention_mfma(a, st),
+          "attention launch");
   return EMA_OK;
 }
 

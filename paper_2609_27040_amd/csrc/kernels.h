@@ -47,11 +47,17 @@ struct AttnArgs {
   int64_t block_bytes;
   int32_t n_local;
   int32_t batch, q_heads, kv_heads, block_size, max_blocks, n_split, dtype;
+  int32_t chunk;            // tokens per workgroup (split size)
   float scale_log2;         // softmax scale times log2(e)
 };
 
-constexpr int kAttnChunk = 256;   // tokens per workgroup (one split)
+constexpr int kAttnChunk = 256;   // tokens per workgroup of the vector-ALU kernel
 
+// Vector-ALU kernel (v_dot2 scores, FMA outputs) plus a separate split-K merge.
 hipError_t launch_paged_attention(const AttnArgs& a, hipStream_t stream);
+// Matrix-core kernel; chunk must be 256 or 512.
+hipError_t launch_paged_attention_mfma(const AttnArgs& a, hipStream_t stream);
+// Merges the split-K partials of sequences longer than one chunk.
+hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t stream);
 
 }  // namespace ema

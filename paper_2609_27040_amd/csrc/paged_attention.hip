@@ -281,30 +281,6 @@ __global__ __launch_bounds__(256) void paged_attn_kernel(AttnArgs a) {
   }
 }
 
-// Merge the split-K partials of one (sequence, query head): 128 threads.
-__global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
-  const int hq = blockIdx.x;
-  const int b = blockIdx.y;
-  const int c = threadIdx.x;
-  const int len = clamp_len(a.seq_lens[b], a);
-  const int nsp = (len + kCh - 1) / kCh;
-  if (nsp <= 1) return;
-  const int64_t base = (int64_t(b) * a.q_heads + hq) * a.n_split;
-  float M = -INFINITY;
-  for (int s = 0; s < nsp; ++s) M = fmaxf(M, a.part_ml[(base + s) * 2]);
-  float L = 0.0f, o = 0.0f;
-  if (M != -INFINITY) {
-    for (int s = 0; s < nsp; ++s) {
-      const float m = a.part_ml[(base + s) * 2];
-      if (m == -INFINITY) continue;
-      const float w = exp2f(m - M);
-      L = fmaf(w, a.part_ml[(base + s) * 2 + 1], L);
-      o = fmaf(w, a.part_o[(base + s) * kD + c], o);
-    }
-  }
-  a.out[(int64_t(b) * a.q_heads + hq) * kD + c] = L > 0.0f ? o / L : 0.0f;
-}
-
 template <int G, int BS>
 hipError_t launch_g_bs(const AttnArgs& a, hipStream_t stream) {
   const dim3 grid(a.n_split, a.kv_heads, a.batch);
@@ -340,12 +316,8 @@ hipError_t launch_paged_attention(const AttnArgs& a, hipStream_t stream) {
     case 16: e = launch_g<16>(a, stream); break;
     default: return hipErrorInvalidValue;
   }
-  if (e != hipSuccess) return e;
-  if (a.n_split > 1) {
-    hipLaunchKernelGGL(attn_combine_kernel, dim3(a.q_heads, a.batch), dim3(128), 0, stream, a);
-    e = hipGetLastError();
-  }
-  return e;
+  if (e != hipSuccess || a.n_split <= 1) return e;
+  return launch_attn_combine(a, stream);
 }
 
 }  // namespace ema

@@ -24,6 +24,17 @@ def ema():
     return m
 
 
+@pytest.fixture(params=["mfma", "valu"])
+def impl(request, monkeypatch):
+    """Attention kernel: the matrix-core one (default) or the vector-ALU one,
+    chosen when the slice is created."""
+    if request.param == "valu":
+        monkeypatch.setenv("EMA_ATTN_KERNEL", "valu")
+    else:
+        monkeypatch.delenv("EMA_ATTN_KERNEL", raising=False)
+    return request.param
+
+
 def oracle_attention(w, st, l):
     return oracle.paged_decode_attention(w.q16, w.attn_tables[l], w.lens, st.read_block, w.hkv,
                                          w.D, w.bs, w.cfg.dtype)
@@ -70,8 +81,8 @@ LENS = [0, 1, 15, 16, 17, 255, 256, 257, 511, 513, 1000, 2049]
 
 
 @pytest.mark.parametrize("hq,hkv,bs,dtype", SHAPES)
-def test_attention_shapes_and_ragged_lengths(ema, hq, hkv, bs, dtype):
-    print(f"attn hq={hq} hkv={hkv} bs={bs} {dtype}", flush=True)
+def test_attention_shapes_and_ragged_lengths(ema, impl, hq, hkv, bs, dtype):
+    print(f"attn {impl} hq={hq} hkv={hkv} bs={bs} {dtype}", flush=True)
     cfg = synth.KVConfig("grid", 1, hq, hkv, 128, dtype, bs, len(LENS), ("uniform", 0, 0), 0.4,
                          31 + bs)
     w = Workload(cfg, lens=LENS, staging_slots=1)
@@ -86,6 +97,55 @@ def test_attention_shapes_and_ragged_lengths(ema, hq, hkv, bs, dtype):
         got = out.cpu().numpy()
         ref = oracle_attention(w, st, 0)
         assert np.all(got[0] == 0.0)                    # empty sequence
+        assert rel_err(got, ref) <= TOL, rel_err(got, ref)
+    finally:
+        w.close()
+
+
+@pytest.mark.parametrize("hq,hkv,bs,dtype,lens", [
+    (8, 1, 32, "bf16", [16384, 12000, 5000, 513, 256, 1]),      # up to 64 splits merged
+    (16, 1, 16, "f16", [9000, 4097, 31]),
+])
+def test_long_sequences_many_splits(ema, impl, hq, hkv, bs, dtype, lens):
+    print(f"long {impl} hq={hq} hkv={hkv} bs={bs} {dtype}", flush=True)
+    cfg = synth.KVConfig("long", 1, hq, hkv, 128, dtype, bs, len(lens), ("uniform", 0, 0), 0.5,
+                         77 + bs)
+    w = Workload(cfg, lens=lens, staging_slots=1)
+    try:
+        st = w.oracle_mirror()
+        w.prefetch(0)
+        st.prefetch(w.pf_src[0], w.pf_dst[0])
+        out = w.new_out()
+        for _ in range(3):                               # counters must reset between calls
+            w.attention(0, out)
+        torch.cuda.synchronize()
+        assert ema.slice_device_errors(w.h) == 0
+        got = out.cpu().numpy()
+        ref = oracle_attention(w, st, 0)
+        assert rel_err(got, ref) <= TOL, rel_err(got, ref)
+    finally:
+        w.close()
+
+
+def test_wide_batch_takes_the_long_chunk_path(ema, impl):
+    """batch x kv heads >= 256 selects 512-token workgroups; full oracle check."""
+    print(f"wide {impl}", flush=True)
+    rng = np.random.default_rng(5)
+    lens = rng.integers(1, 3000, 32).tolist()
+    lens[:4] = [0, 1, 512, 513]
+    cfg = synth.KVConfig("wide", 1, 32, 8, 128, "bf16", 16, 32, ("uniform", 0, 0), 0.3, 91)
+    w = Workload(cfg, lens=lens, staging_slots=1)
+    try:
+        st = w.oracle_mirror()
+        w.prefetch(0)
+        st.prefetch(w.pf_src[0], w.pf_dst[0])
+        out = w.new_out()
+        w.attention(0, out)
+        torch.cuda.synchronize()
+        assert ema.slice_device_errors(w.h) == 0
+        got = out.cpu().numpy()
+        assert np.all(got[0] == 0.0)
+        ref = oracle_attention(w, st, 0)
         assert rel_err(got, ref) <= TOL, rel_err(got, ref)
     finally:
         w.close()
