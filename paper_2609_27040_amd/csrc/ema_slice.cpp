@@ -38,6 +38,7 @@ struct ema_slice {
   float* d_part = nullptr;
   size_t part_cap = 0;          // floats
   bool attn_valu = false;         // EMA_ATTN_KERNEL=valu selects the vector-ALU kernel
+  int32_t attn_chunk = 0;         // EMA_ATTN_CHUNK=256|512|1024 overrides the split size
 };
 
 namespace {
@@ -148,6 +149,10 @@ int ema_slice_create(const ema_kv_shape* shape, size_t local_bytes, size_t lent_
   h->checked = (flags & EMA_CREATE_CHECKED) != 0;
   const char* impl = std::getenv("EMA_ATTN_KERNEL");
   h->attn_valu = impl && std::strcmp(impl, "valu") == 0;
+  if (const char* c = std::getenv("EMA_ATTN_CHUNK")) {
+    const int v = std::atoi(c);
+    if (v == 256 || v == 512 || v == 1024) h->attn_chunk = v;
+  }
   h->book.init(int32_t(nl), int32_t(ns));
   if (h->host_only) {
     *out = h;
@@ -360,6 +365,7 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
   const int64_t max_tokens = int64_t(max_blocks) * h->shape.block_size;
   if (max_tokens > (1LL << 30)) return fail(EMA_ERR_INVAL, "attention: max_blocks too large");
   if (h->host_only || batch == 0) return EMA_OK;
+  if (h->book.n_local() == 0) return fail(EMA_ERR_INVAL, "attention: the local pool is empty");
   int rc = use_device(h);
   if (rc) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -379,11 +385,11 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
       }
     }
   }
-  // Tokens per workgroup: the vector-ALU kernel uses a fixed chunk; the
-  // matrix-core kernel takes 512-token chunks when there are enough
-  // (sequence, KV head) pairs to fill the GPU, else 256 for more splits.
-  const int32_t chunk = h->attn_valu ? ema::kAttnChunk
-                                     : (int64_t(batch) * hkv >= 256 ? 512 : 256);
+  // Tokens per work item (split-K chunk): fixed for the vector-ALU kernel;
+  // 512 for the matrix-core kernel, whose persistent workgroups balance the
+  // items themselves.
+  int32_t chunk = h->attn_valu ? ema::kAttnChunk : 512;
+  if (!h->attn_valu && h->attn_chunk) chunk = h->attn_chunk;
   const int32_t n_split = int32_t(std::max<int64_t>(1, (max_tokens + chunk - 1) / chunk));
   if (n_split > 65535) return fail(EMA_ERR_INVAL, "attention: max_blocks too large");
   if (n_split > 1) {

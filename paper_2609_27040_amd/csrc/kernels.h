@@ -55,7 +55,7 @@ constexpr int kAttnChunk = 256;   // tokens per workgroup of the vector-ALU kern
 
 // Vector-ALU kernel (v_dot2 scores, FMA outputs) plus a separate split-K merge.
 hipError_t launch_paged_attention(const AttnArgs& a, hipStream_t stream);
-// Matrix-core kernel; chunk must be 256 or 512.
+// Matrix-core kernel; chunk must be 256, 512 or 1024.
 hipError_t launch_paged_attention_mfma(const AttnArgs& a, hipStream_t stream);
 // Merges the split-K partials of sequences longer than one chunk.
 hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t stream);

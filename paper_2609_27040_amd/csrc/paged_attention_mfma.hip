@@ -26,6 +26,7 @@
 // Reduction orders depend only on sequence lengths, not on block ids.
 #include "kernels.h"
 
+#include <algorithm>
 #include <cmath>
 
 namespace ema {
@@ -40,7 +41,8 @@ constexpr int kD = 128;
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kIt = 32;                 // tokens per wave iteration
-constexpr int kMaxIds = 512 / 16;       // block ids of the largest chunk at the smallest block
+constexpr int kMaxIds = 1024 / 16;      // block ids of the largest chunk at the smallest block
+constexpr int kMaxPersistBatch = 2048;  // sequences the persistent work list holds in LDS
 
 __device__ __forceinline__ u32x4 ld16(const char* p) {
   return *reinterpret_cast<const u32x4*>(p);
@@ -78,15 +80,114 @@ __device__ __forceinline__ int clamp_len(int len, const AttnArgs& a) {
   return len < 0 ? 0 : (len > cap ? cap : len);
 }
 
-template <int G, int BS, bool BF16>
-__global__ __launch_bounds__(kThreads, 3) void attn_mfma_kernel(AttnArgs a) {
-  __shared__ int32_t s_ids[kMaxIds];
-  __shared__ __attribute__((aligned(16))) float s_o[kWaves][G][kD];
-  __shared__ float s_m[kWaves][G], s_l[kWaves][G];
+// One 32-token iteration's operands: K rows of the two score tiles and the
+// eight V^T row tiles, plus how many of this lane's 8 tokens are valid.
+struct Tile {
+  u32x4 k[2][4];
+  u32x4 v[8];
+  int nv;
+};
 
-  const int split = blockIdx.x;
-  const int kvh = blockIdx.y;
-  const int b = blockIdx.z;
+// Issues the loads of the iteration starting at chunk token t0. Every lane
+// loads unconditionally (a lane whose token is masked reads block 0, which
+// always exists), so the loads stay in straight-line code and the compiler can
+// wait for this tile alone while the next one is in flight. K rows of masked
+// tokens only reach scores that consume_tile sets to -inf; V of masked tokens
+// is zeroed there before use.
+template <int BS>
+__device__ __forceinline__ void load_tile(Tile& T, int t0, int nvalid, const int32_t* s_ids,
+                                          const char* pool, int64_t Bb, int kvh, int r16,
+                                          int q4) {
+  // K rows: tile t, row r16 -> token t0 + 8*(r16/4) + 4t + r16%4.
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int tok = t0 + 8 * (r16 >> 2) + 4 * t + (r16 & 3);
+    const int id = s_ids[tok / BS];
+    const bool ok = tok < nvalid && id >= 0;
+    const char* p = pool + (ok ? int64_t(id) * Bb + (int64_t(kvh * BS + tok % BS) * kD + q4 * 8) * 2
+                               : int64_t(0));
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) T.k[t][kk] = ld16(p + kk * 64);
+  }
+  // V^T rows: d-tile n, row 16n + r16, tokens t0 + 8q4 .. +8 (one block).
+  const int vt = t0 + 8 * q4;
+  const int vid = s_ids[vt / BS];
+  const int vleft = nvalid - vt;
+  T.nv = vid < 0 ? 0 : (vleft < 0 ? 0 : (vleft > 8 ? 8 : vleft));
+  const char* p = pool + (T.nv > 0 ? int64_t(vid) * Bb + Bb / 2 +
+                                         (int64_t(kvh * kD + r16) * BS + vt % BS) * 2
+                                   : int64_t(0));
+#pragma unroll
+  for (int n = 0; n < 8; ++n) T.v[n] = ld16(p + int64_t(16 * n) * BS * 2);
+}
+
+// Scores, online softmax update and P.V for one loaded iteration.
+// `issue_next` runs right after the score products are issued: loads of the
+// next tile then queue behind this tile's V loads, so the in-order wait
+// before P.V covers this tile only.
+template <bool BF16, typename Next>
+__device__ __forceinline__ void consume_tile(Tile& T, const u32x4 (&qb)[4], float scale_log2,
+                                             float& m, float& lsum, f32x4 (&o)[8],
+                                             Next&& issue_next) {
+  const int nv = T.nv;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {   // branch-free, so waits stay per tile
+    const uint32_t keep = (2 * q < nv ? 0xffffu : 0u) | (2 * q + 1 < nv ? 0xffff0000u : 0u);
+#pragma unroll
+    for (int n = 0; n < 8; ++n) T.v[n][q] &= keep;
+  }
+  // Scores for tokens 8q4 + 4t + i of head r16.
+  f32x4 s[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    s[t] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) s[t] = mfma<BF16>(T.k[t][kk], qb[kk], s[t]);
+  }
+  issue_next();
+  float sv[8];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    sv[j] = j < nv ? s[j >> 2][j & 3] * scale_log2 : -INFINITY;
+    mx = fmaxf(mx, sv[j]);
+  }
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const float m_new = fmaxf(m, mx);
+  const float alpha = m_new == -INFINITY ? 1.0f : exp2f(m - m_new);
+  uint32_t ph[4], pl[4];
+  float ps = 0.0f;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float p0 = m_new == -INFINITY ? 0.0f : exp2f(sv[2 * q] - m_new);
+    const float p1 = m_new == -INFINITY ? 0.0f : exp2f(sv[2 * q + 1] - m_new);
+    ps += p0 + p1;
+    uint32_t h0, l0, h1, l1;
+    split16<BF16>(p0, h0, l0);
+    split16<BF16>(p1, h1, l1);
+    ph[q] = h0 | (h1 << 16);
+    pl[q] = l0 | (l1 << 16);
+  }
+  lsum = lsum * alpha + ps;
+  m = m_new;
+  const u32x4 PH = {ph[0], ph[1], ph[2], ph[3]};
+  const u32x4 PL = {pl[0], pl[1], pl[2], pl[3]};
+#pragma unroll
+  for (int n = 0; n < 8; ++n) {
+    o[n] *= alpha;
+    o[n] = mfma<BF16>(T.v[n], PH, o[n]);
+    o[n] = mfma<BF16>(T.v[n], PL, o[n]);
+  }
+}
+
+// One work item: chunk `split` of sequence b (length len > split*chunk) for
+// KV head kvh. All threads of the workgroup take part; the LDS buffers are
+// reused by the next item (the barrier after the id load separates them).
+template <int G, int BS, bool BF16>
+__device__ __forceinline__ void process_item(const AttnArgs& a, int b, int kvh, int split,
+                                             int len, int32_t* s_ids, float (*s_o)[G][kD],
+                                             float (*s_m)[G], float (*s_l)[G]) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -94,24 +195,14 @@ __global__ __launch_bounds__(kThreads, 3) void attn_mfma_kernel(AttnArgs a) {
   const int q4 = lane >> 4;
   const int Hq = a.q_heads;
   const int chunk = a.chunk;
-
-  const int raw_len = a.seq_lens[b];
-  const int len = clamp_len(raw_len, a);
-  if (split == 0 && kvh == 0 && tid == 0 && len != raw_len && raw_len > 0)
-    atomicAdd(a.err_count, 1);
-  if (len == 0) {
-    if (split == 0)
-      for (int e = tid; e < G * kD; e += kThreads)
-        a.out[(int64_t(b) * Hq + kvh * G + e / kD) * kD + (e % kD)] = 0.0f;
-    return;
-  }
   const int n_split_b = (len + chunk - 1) / chunk;
-  if (split >= n_split_b) return;
   const int c_start = split * chunk;
   const int nvalid = min(chunk, len - c_start);
   const int nb = chunk / BS;
-  for (int i = tid; i < nb; i += kThreads) {
-    const int j = c_start / BS + i;
+
+  // Block ids of the chunk and q are loaded together (one memory round trip).
+  if (tid < nb) {
+    const int j = c_start / BS + tid;
     int id = -1;
     if (j * BS < len) {
       id = a.table[int64_t(b) * a.max_blocks + j];
@@ -120,13 +211,8 @@ __global__ __launch_bounds__(kThreads, 3) void attn_mfma_kernel(AttnArgs a) {
         id = -1;
       }
     }
-    s_ids[i] = id;
+    s_ids[tid] = id;
   }
-  __syncthreads();
-
-  const char* pool = a.local;
-  const int64_t Bb = a.block_bytes;
-
   // Q^T as the B operand: lane (head r16, q4) holds channels 32kk + 8q4 .. +8.
   u32x4 qb[4];
   {
@@ -136,92 +222,33 @@ __global__ __launch_bounds__(kThreads, 3) void attn_mfma_kernel(AttnArgs a) {
     for (int kk = 0; kk < 4; ++kk)
       qb[kk] = r16 < G ? ld16(qrow + kk * 64) : u32x4{0, 0, 0, 0};
   }
+  __syncthreads();
 
+  const char* pool = a.local;
+  const int64_t Bb = a.block_bytes;
   float m = -INFINITY;   // running max of this lane's head (log2 domain)
   float lsum = 0.0f;     // this lane's share of the running sum
   f32x4 o[8];
 #pragma unroll
   for (int n = 0; n < 8; ++n) o[n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
+  // Iterations of this wave that hold valid tokens; loads run one ahead.
   const int its = chunk / (kWaves * kIt);
-  for (int it = 0; it < its; ++it) {
-    const int t0 = (wave * its + it) * kIt;
-    if (t0 >= nvalid) break;
-    // K rows: tile t, row r16 -> token t0 + 8*(r16/4) + 4t + r16%4.
-    u32x4 kr[2][4];
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int tok = t0 + 8 * (r16 >> 2) + 4 * t + (r16 & 3);
-      const int id = s_ids[tok / BS];
-      const bool ok = tok < nvalid && id >= 0;
-      const char* p = pool + int64_t(ok ? id : 0) * Bb +
-                      (int64_t(kvh * BS + tok % BS) * kD + q4 * 8) * 2;
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) kr[t][kk] = ok ? ld16(p + kk * 64) : u32x4{0, 0, 0, 0};
-    }
-    // V^T rows: d-tile n, row 16n + r16, tokens t0 + 8q4 .. +8 (one block).
-    const int vt = t0 + 8 * q4;
-    const int vid = s_ids[vt / BS];
-    const int vleft = nvalid - vt;
-    const int nv = vid < 0 ? 0 : (vleft < 0 ? 0 : (vleft > 8 ? 8 : vleft));
-    u32x4 vr[8];
-    {
-      const char* p = pool + int64_t(nv > 0 ? vid : 0) * Bb + Bb / 2 +
-                      (int64_t(kvh * kD + r16) * BS + vt % BS) * 2;
-#pragma unroll
-      for (int n = 0; n < 8; ++n)
-        vr[n] = nv > 0 ? ld16(p + int64_t(16 * n) * BS * 2) : u32x4{0, 0, 0, 0};
-      if (nv > 0 && nv < 8) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const uint32_t keep = (2 * q < nv ? 0xffffu : 0u) | (2 * q + 1 < nv ? 0xffff0000u : 0u);
-#pragma unroll
-          for (int n = 0; n < 8; ++n) vr[n][q] &= keep;
-        }
-      }
-    }
-    // Scores for tokens vt + 4t + i of head r16.
-    f32x4 s[2];
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      s[t] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) s[t] = mfma<BF16>(kr[t][kk], qb[kk], s[t]);
-    }
-    float sv[8];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      sv[j] = j < nv ? s[j >> 2][j & 3] * a.scale_log2 : -INFINITY;
-      mx = fmaxf(mx, sv[j]);
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m, mx);
-    const float alpha = m_new == -INFINITY ? 1.0f : exp2f(m - m_new);
-    uint32_t ph[4], pl[4];
-    float ps = 0.0f;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float p0 = m_new == -INFINITY ? 0.0f : exp2f(sv[2 * q] - m_new);
-      const float p1 = m_new == -INFINITY ? 0.0f : exp2f(sv[2 * q + 1] - m_new);
-      ps += p0 + p1;
-      uint32_t h0, l0, h1, l1;
-      split16<BF16>(p0, h0, l0);
-      split16<BF16>(p1, h1, l1);
-      ph[q] = h0 | (h1 << 16);
-      pl[q] = l0 | (l1 << 16);
-    }
-    lsum = lsum * alpha + ps;
-    m = m_new;
-    const u32x4 PH = {ph[0], ph[1], ph[2], ph[3]};
-    const u32x4 PL = {pl[0], pl[1], pl[2], pl[3]};
-#pragma unroll
-    for (int n = 0; n < 8; ++n) {
-      o[n] *= alpha;
-      o[n] = mfma<BF16>(vr[n], PH, o[n]);
-      o[n] = mfma<BF16>(vr[n], PL, o[n]);
-    }
+  const int w0 = wave * its * kIt;
+  const int n_it = nvalid <= w0 ? 0 : min(its, (nvalid - w0 + kIt - 1) / kIt);
+  Tile A, B;
+  auto load_at = [&](Tile& T, int it) {
+    load_tile<BS>(T, w0 + it * kIt, nvalid, s_ids, pool, Bb, kvh, r16, q4);
+  };
+  if (n_it > 0) load_at(A, 0);
+  for (int it = 0; it < n_it; it += 2) {
+    consume_tile<BF16>(A, qb, a.scale_log2, m, lsum, o, [&] {
+      if (it + 1 < n_it) load_at(B, it + 1);
+    });
+    if (it + 1 >= n_it) break;
+    consume_tile<BF16>(B, qb, a.scale_log2, m, lsum, o, [&] {
+      if (it + 2 < n_it) load_at(A, it + 2);
+    });
   }
 
   // ---- merge the four waves ------------------------------------------------
@@ -269,14 +296,128 @@ __global__ __launch_bounds__(kThreads, 3) void attn_mfma_kernel(AttnArgs a) {
   }
 }
 
+__device__ __forceinline__ void write_zeros(const AttnArgs& a, int b) {
+  for (int e = threadIdx.x; e < a.q_heads * kD; e += kThreads)
+    a.out[int64_t(b) * a.q_heads * kD + e] = 0.0f;
+}
+
+// Persistent form: gridDim.x workgroups (as many as stay resident) share the
+// work list. Each reads every sequence length once, counts its chunks,
+// prefix-sums the counts in LDS and then takes items blockIdx.x,
+// blockIdx.x + gridDim.x, ... ; item i -> (sequence, chunk, KV head) with the
+// KV head fastest. No workgroup is launched only to find it has no work.
+template <int G, int BS, bool BF16>
+__global__ __launch_bounds__(kThreads, 2) void attn_mfma_persistent(AttnArgs a) {
+  __shared__ int32_t s_ids[kMaxIds];
+  __shared__ __attribute__((aligned(16))) float s_o[kWaves][G][kD];
+  __shared__ float s_m[kWaves][G], s_l[kWaves][G];
+  __shared__ int32_t s_len[kMaxPersistBatch];
+  __shared__ int32_t s_pref[kMaxPersistBatch + 1];
+  __shared__ int32_t s_seg[kThreads];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int B = a.batch;
+  const int H = a.kv_heads;
+  const int chunk = a.chunk;
+  const int per = (B + kThreads - 1) / kThreads;
+  const int b0 = min(B, tid * per);
+  const int b1 = min(B, b0 + per);
+  int run = 0;
+  for (int b = b0; b < b1; ++b) {
+    const int raw = a.seq_lens[b];
+    const int len = clamp_len(raw, a);
+    if (blockIdx.x == 0 && len != raw && raw > 0) atomicAdd(a.err_count, 1);
+    s_len[b] = len;
+    s_pref[b] = run;
+    run += (len + chunk - 1) / chunk * H;
+  }
+  s_seg[tid] = run;
+  __syncthreads();
+  if (tid < 64) {   // exclusive scan of the 256 segment totals
+    const int v0 = s_seg[4 * lane], v1 = s_seg[4 * lane + 1];
+    const int v2 = s_seg[4 * lane + 2], v3 = s_seg[4 * lane + 3];
+    int sum = v0 + v1 + v2 + v3;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(sum, o);
+      if (lane >= o) sum += t;
+    }
+    const int ex = sum - (v0 + v1 + v2 + v3);
+    s_seg[4 * lane] = ex;
+    s_seg[4 * lane + 1] = ex + v0;
+    s_seg[4 * lane + 2] = ex + v0 + v1;
+    s_seg[4 * lane + 3] = ex + v0 + v1 + v2;
+    if (lane == 63) s_pref[B] = sum;
+  }
+  __syncthreads();
+  for (int b = b0; b < b1; ++b) s_pref[b] += s_seg[tid];
+  __syncthreads();
+  for (int b = blockIdx.x; b < B; b += gridDim.x)
+    if (s_len[b] == 0) write_zeros(a, b);
+  const int total = s_pref[B];
+  for (int item = blockIdx.x; item < total; item += gridDim.x) {
+    int lo = 0, hi = B - 1;   // last sequence whose first item is <= item
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (s_pref[mid] <= item) lo = mid;
+      else hi = mid - 1;
+    }
+    const int r = item - s_pref[lo];
+    process_item<G, BS, BF16>(a, lo, r % H, r / H, s_len[lo], s_ids, s_o, s_m, s_l);
+  }
+}
+
+// Grid form for batches too large for the persistent work list:
+// grid (chunk, KV head, sequence); workgroups past a sequence's end exit.
+template <int G, int BS, bool BF16>
+__global__ __launch_bounds__(kThreads, 2) void attn_mfma_grid(AttnArgs a) {
+  __shared__ int32_t s_ids[kMaxIds];
+  __shared__ __attribute__((aligned(16))) float s_o[kWaves][G][kD];
+  __shared__ float s_m[kWaves][G], s_l[kWaves][G];
+  const int split = blockIdx.x;
+  const int kvh = blockIdx.y;
+  const int b = blockIdx.z;
+  const int raw = a.seq_lens[b];
+  const int len = clamp_len(raw, a);
+  if (split == 0 && kvh == 0 && threadIdx.x == 0 && len != raw && raw > 0)
+    atomicAdd(a.err_count, 1);
+  if (len == 0) {
+    if (split == 0 && kvh == 0) write_zeros(a, b);
+    return;
+  }
+  if (split >= (len + a.chunk - 1) / a.chunk) return;
+  process_item<G, BS, BF16>(a, b, kvh, split, len, s_ids, s_o, s_m, s_l);
+}
+
+template <typename K>
+int resident_workgroups(K kernel) {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0) != hipSuccess)
+    return 0;
+  return cus * (per_cu > 0 ? per_cu : 1);
+}
+
+template <int G, int BS, bool BF16>
+hipError_t launch_typed(const AttnArgs& a, hipStream_t stream) {
+  if (a.batch <= kMaxPersistBatch) {
+    static const int resident = resident_workgroups(attn_mfma_persistent<G, BS, BF16>);
+    const int64_t upper = int64_t(a.batch) * a.kv_heads * a.n_split;
+    const int grid = int(std::max<int64_t>(1, std::min<int64_t>(resident > 0 ? resident : 512,
+                                                                 upper)));
+    hipLaunchKernelGGL((attn_mfma_persistent<G, BS, BF16>), dim3(grid), dim3(kThreads), 0,
+                       stream, a);
+  } else {
+    hipLaunchKernelGGL((attn_mfma_grid<G, BS, BF16>), dim3(a.n_split, a.kv_heads, a.batch),
+                       dim3(kThreads), 0, stream, a);
+  }
+  return hipGetLastError();
+}
+
 template <int G, int BS>
 hipError_t launch_g_bs(const AttnArgs& a, hipStream_t stream) {
-  const dim3 grid(a.n_split, a.kv_heads, a.batch);
-  if (a.dtype == 1)
-    hipLaunchKernelGGL((attn_mfma_kernel<G, BS, true>), grid, dim3(kThreads), 0, stream, a);
-  else
-    hipLaunchKernelGGL((attn_mfma_kernel<G, BS, false>), grid, dim3(kThreads), 0, stream, a);
-  return hipGetLastError();
+  return a.dtype == 1 ? launch_typed<G, BS, true>(a, stream) : launch_typed<G, BS, false>(a, stream);
 }
 
 template <int G>

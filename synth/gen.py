@@ -57,10 +57,11 @@ class BlockPlacement:
     slice_order: np.ndarray
 
 
-def placement(cfg, lens, rng, frac=None, layers=None) -> BlockPlacement:
+def placement(cfg, lens, rng, frac=None, layers=None, shuffle=True) -> BlockPlacement:
     """Pick, per layer, exactly round(frac * n_l) of the layer's n_l logical
     blocks (uniform, without replacement) to live in the slice, and a random
-    allocation order for each pool."""
+    allocation order for each pool (``shuffle=False``: layer-major order, as in
+    a freshly filled cache)."""
     frac = cfg.slice_frac if frac is None else frac
     L = cfg.layers if layers is None else layers
     bs = cfg.block_size
@@ -81,8 +82,9 @@ def placement(cfg, lens, rng, frac=None, layers=None) -> BlockPlacement:
     sl = in_slice[all_l, all_b, all_j]
     loc = np.stack([all_l[~sl], all_b[~sl], all_j[~sl]], axis=1)
     sli = np.stack([all_l[sl], all_b[sl], all_j[sl]], axis=1)
-    loc = loc[rng.permutation(len(loc))]
-    sli = sli[rng.permutation(len(sli))]
+    if shuffle:
+        loc = loc[rng.permutation(len(loc))]
+        sli = sli[rng.permutation(len(sli))]
     return BlockPlacement(nblocks, maxblk, in_slice, loc, sli)
 
 

@@ -25,13 +25,14 @@ TORCH_DT = {"f16": torch.float16, "bf16": torch.bfloat16}
 class Workload:
     def __init__(self, cfg, layers=None, batch=None, slice_layout=ema.LAYOUT_ATTN, seed=None,
                  staging_slots=2, extra_local=0, extra_slice=0, fill="host", checked=False,
-                 lens=None, frac=None):
+                 lens=None, frac=None, shuffle=True):
         self.cfg = cfg = cfg if batch is None else cfg.scaled(batch=batch)
         self.L = cfg.layers if layers is None else layers
         rng = np.random.default_rng(cfg.seed if seed is None else seed)
         self.lens = synth.seq_lens(cfg, rng) if lens is None else np.asarray(lens, np.int64)
         self.B = len(self.lens)
-        self.pl = pl = synth.placement(cfg, self.lens, rng, frac=frac, layers=self.L)
+        self.pl = pl = synth.placement(cfg, self.lens, rng, frac=frac, layers=self.L,
+                                       shuffle=shuffle)
         self.bs, self.hkv, self.D = cfg.block_size, cfg.kv_heads, cfg.head_dim
         self.bb = cfg.block_bytes
         self.maxblk = max(pl.maxblk, 1)
