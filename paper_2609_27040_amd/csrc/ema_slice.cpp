@@ -37,8 +37,10 @@ struct ema_slice {
   bool h_work_pending = false;
   float* d_part = nullptr;
   size_t part_cap = 0;          // floats
+  int32_t* d_info = nullptr;      // stream-K: per (sequence, KV head) partial ranges
+  size_t info_cap = 0;            // ints
   bool attn_valu = false;         // EMA_ATTN_KERNEL=valu selects the vector-ALU kernel
-  int32_t attn_chunk = 0;         // EMA_ATTN_CHUNK=256|512|1024 overrides the split size
+  bool attn_grid = false;         // EMA_ATTN_SCHED=grid forces the matrix-core grid form
 };
 
 namespace {
@@ -115,6 +117,7 @@ void release(ema_slice* h) {
     if (h->d_err) (void)hipFree(h->d_err);
     if (h->d_work) (void)hipFree(h->d_work);
     if (h->d_part) (void)hipFree(h->d_part);
+    if (h->d_info) (void)hipFree(h->d_info);
     if (h->h_work) (void)hipHostFree(h->h_work);
     if (h->h_work_ev) (void)hipEventDestroy(h->h_work_ev);
   }
@@ -149,10 +152,8 @@ int ema_slice_create(const ema_kv_shape* shape, size_t local_bytes, size_t lent_
   h->checked = (flags & EMA_CREATE_CHECKED) != 0;
   const char* impl = std::getenv("EMA_ATTN_KERNEL");
   h->attn_valu = impl && std::strcmp(impl, "valu") == 0;
-  if (const char* c = std::getenv("EMA_ATTN_CHUNK")) {
-    const int v = std::atoi(c);
-    if (v == 256 || v == 512 || v == 1024) h->attn_chunk = v;
-  }
+  const char* sched = std::getenv("EMA_ATTN_SCHED");
+  h->attn_grid = sched && std::strcmp(sched, "grid") == 0;
   h->book.init(int32_t(nl), int32_t(ns));
   if (h->host_only) {
     *out = h;
@@ -385,25 +386,36 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
       }
     }
   }
-  // Tokens per work item (split-K chunk): fixed for the vector-ALU kernel;
-  // 512 for the matrix-core kernel, whose persistent workgroups balance the
-  // items themselves.
-  int32_t chunk = h->attn_valu ? ema::kAttnChunk : 512;
-  if (!h->attn_valu && h->attn_chunk) chunk = h->attn_chunk;
+  // Scheduling. Matrix-core kernel: stream-K (equal tile ranges per resident
+  // workgroup, at most two partials each) when the batch fits its LDS work
+  // list, else a grid of 1024-token chunks. Vector-ALU kernel: a grid of
+  // 256-token chunks. Grid forms keep one partial per (sequence, head, chunk).
+  const int64_t tiles = int64_t(batch) * hkv * ((max_tokens + 31) / 32);
+  const bool stream_k = !h->attn_valu && !h->attn_grid && batch <= ema::kStreamKMaxBatch &&
+                        tiles < (int64_t(1) << 30);
+  const int32_t chunk = h->attn_valu ? ema::kAttnChunk : ema::kMfmaGridChunk;
   const int32_t n_split = int32_t(std::max<int64_t>(1, (max_tokens + chunk - 1) / chunk));
-  if (n_split > 65535) return fail(EMA_ERR_INVAL, "attention: max_blocks too large");
-  if (n_split > 1) {
-    const size_t rows = size_t(batch) * num_q_heads * n_split;
-    if ((rc = grow_device(reinterpret_cast<void**>(&h->d_part), &h->part_cap, rows * 130, 4)))
-      return rc;
-  }
+  if (!stream_k && n_split > 65535) return fail(EMA_ERR_INVAL, "attention: max_blocks too large");
+  size_t part_rows = 0;
+  if (stream_k)
+    part_rows = size_t(2) * ema::kMaxStreamGrid * G;
+  else if (n_split > 1)
+    part_rows = size_t(batch) * num_q_heads * n_split;
+  if (part_rows &&
+      (rc = grow_device(reinterpret_cast<void**>(&h->d_part), &h->part_cap, part_rows * 130, 4)))
+    return rc;
+  if (stream_k && (rc = grow_device(reinterpret_cast<void**>(&h->d_info), &h->info_cap,
+                                    size_t(batch) * hkv * 3, 4)))
+    return rc;
   ema::AttnArgs a;
   a.q = q;
   a.table = block_table;
   a.seq_lens = seq_lens;
   a.out = out;
   a.part_o = h->d_part;
-  a.part_ml = h->d_part ? h->d_part + size_t(batch) * num_q_heads * n_split * 128 : nullptr;
+  a.part_ml = h->d_part ? h->d_part + part_rows * 128 : nullptr;
+  a.info = h->d_info;
+  a.stream_k = stream_k ? 1 : 0;
   a.err_count = h->d_err;
   a.local = h->local;
   a.block_bytes = h->bb;

@@ -42,20 +42,27 @@ struct AttnArgs {
   float* out;               // [B][Hq][128]
   float* part_o;            // [B][Hq][n_split][128] split-K partial outputs
   float* part_ml;           // [B][Hq][n_split][2] running max (log2 domain) and sum
+                            // (stream-K: [2 * grid][G][...] partial slots instead)
+  int32_t* info;            // stream-K: [B][Hkv][3] first / last workgroup, first slot
   int32_t* err_count;
   const char* local;        // local pool base
   int64_t block_bytes;
   int32_t n_local;
   int32_t batch, q_heads, kv_heads, block_size, max_blocks, n_split, dtype;
-  int32_t chunk;            // tokens per workgroup (split size)
+  int32_t chunk;            // tokens per split (grid forms)
+  int32_t stream_k;         // matrix-core kernel: stream-K scheduling (else grid form)
   float scale_log2;         // softmax scale times log2(e)
 };
 
-constexpr int kAttnChunk = 256;   // tokens per workgroup of the vector-ALU kernel
+constexpr int kAttnChunk = 256;        // tokens per workgroup of the vector-ALU kernel
+constexpr int kMfmaGridChunk = 1024;   // tokens per workgroup of the matrix-core grid form
+constexpr int kStreamKMaxBatch = 2048; // sequences the stream-K work list holds
+constexpr int kMaxStreamGrid = 2048;   // stream-K workgroups (partial slots: 2 each)
 
 // Vector-ALU kernel (v_dot2 scores, FMA outputs) plus a separate split-K merge.
 hipError_t launch_paged_attention(const AttnArgs& a, hipStream_t stream);
-// Matrix-core kernel; chunk must be 256, 512 or 1024.
+// Matrix-core kernel: stream-K when stream_k is set, else the grid form with
+// chunk == kMfmaGridChunk.
 hipError_t launch_paged_attention_mfma(const AttnArgs& a, hipStream_t stream);
 // Merges the split-K partials of sequences longer than one chunk.
 hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t stream);

@@ -6,8 +6,8 @@
 // v_mfma_f32_16x16x32_{bf16,f16} (G <= 16 heads fill one 16-wide tile), which
 // leaves the vector ALUs nearly idle and the kernel bound by HBM.
 //
-// Grid (chunk, KV head, sequence), 4 wavefronts. Each wavefront streams
-// 32-token iterations of its share of the chunk with an online softmax:
+// Work is cut into 32-token tiles of one (sequence, KV head). Each wavefront
+// streams tiles with an online softmax, two tiles in flight:
 //   scores   S^T[token][head] = K . Q^T   (A = 16 K rows straight from the
 //            block, B = Q^T held in registers; two 16-token tiles whose rows
 //            are chosen so that each lane ends up holding 8 consecutive
@@ -17,11 +17,15 @@
 //            transposed V block, 8 consecutive tokens per lane, 16 B loads;
 //            P is split into a 16-bit high part and a 16-bit remainder so the
 //            probabilities keep ~16 significant bits)
-// The four waves' (max, sum, output) are merged in LDS. A sequence longer
-// than one chunk writes a partial (unnormalised output, max, sum) that the
-// split-K combine kernel merges; merging in-kernel would need device-scope
-// fences, which write back and invalidate the whole L2 of an XCD per
-// workgroup on this chip. Masked tokens (past the length, or in a block whose id is out of
+// Scheduling is stream-K: the tiles of all (sequence, KV head) pairs, in that
+// order, are split into equal contiguous ranges, one per resident workgroup
+// (4 wavefronts), so every workgroup streams the same number of bytes
+// whatever the length mix. A workgroup keeps its softmax state across the
+// tiles of one (sequence, KV head); a pair it covers whole is written out
+// directly, a pair cut by a range boundary leaves one partial per workgroup
+// (unnormalised output, max, sum) that a small combine kernel merges. Merging
+// in-kernel would need device-scope fences, which write back and invalidate an
+// XCD's whole L2 per workgroup on this chip. Masked tokens (past the length, or in a block whose id is out of
 // range) get -inf scores and zeroed V, so NaN in unused slots never leaks.
 // Reduction orders depend only on sequence lengths, not on block ids.
 #include "kernels.h"
@@ -40,9 +44,11 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int kD = 128;
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
-constexpr int kIt = 32;                 // tokens per wave iteration
-constexpr int kMaxIds = 1024 / 16;      // block ids of the largest chunk at the smallest block
-constexpr int kMaxPersistBatch = 2048;  // sequences the persistent work list holds in LDS
+constexpr int kIt = 32;                    // tokens per tile (one wave iteration)
+constexpr int kPieceTiles = 32;            // tiles whose block ids are staged in LDS at once
+constexpr int kMaxIds = kPieceTiles * kIt / 16;
+constexpr int kMaxPersistBatch = 2048;     // sequences the stream-K work list holds in LDS
+constexpr int kGridChunkTiles = 32;        // tiles per workgroup in the grid fallback
 
 __device__ __forceinline__ u32x4 ld16(const char* p) {
   return *reinterpret_cast<const u32x4*>(p);
@@ -88,22 +94,22 @@ struct Tile {
   int nv;
 };
 
-// Issues the loads of the iteration starting at chunk token t0. Every lane
+// Issues the loads of the tile starting at token t0 of the sequence. Every lane
 // loads unconditionally (a lane whose token is masked reads block 0, which
 // always exists), so the loads stay in straight-line code and the compiler can
 // wait for this tile alone while the next one is in flight. K rows of masked
 // tokens only reach scores that consume_tile sets to -inf; V of masked tokens
 // is zeroed there before use.
 template <int BS>
-__device__ __forceinline__ void load_tile(Tile& T, int t0, int nvalid, const int32_t* s_ids,
+__device__ __forceinline__ void load_tile(Tile& T, int t0, int len, int blk0, const int32_t* s_ids,
                                           const char* pool, int64_t Bb, int kvh, int r16,
                                           int q4) {
   // K rows: tile t, row r16 -> token t0 + 8*(r16/4) + 4t + r16%4.
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
     const int tok = t0 + 8 * (r16 >> 2) + 4 * t + (r16 & 3);
-    const int id = s_ids[tok / BS];
-    const bool ok = tok < nvalid && id >= 0;
+    const int id = s_ids[tok / BS - blk0];
+    const bool ok = tok < len && id >= 0;
     const char* p = pool + (ok ? int64_t(id) * Bb + (int64_t(kvh * BS + tok % BS) * kD + q4 * 8) * 2
                                : int64_t(0));
 #pragma unroll
@@ -111,8 +117,8 @@ __device__ __forceinline__ void load_tile(Tile& T, int t0, int nvalid, const int
   }
   // V^T rows: d-tile n, row 16n + r16, tokens t0 + 8q4 .. +8 (one block).
   const int vt = t0 + 8 * q4;
-  const int vid = s_ids[vt / BS];
-  const int vleft = nvalid - vt;
+  const int vid = s_ids[vt / BS - blk0];
+  const int vleft = len - vt;
   T.nv = vid < 0 ? 0 : (vleft < 0 ? 0 : (vleft > 8 ? 8 : vleft));
   const char* p = pool + (T.nv > 0 ? int64_t(vid) * Bb + Bb / 2 +
                                          (int64_t(kvh * kD + r16) * BS + vt % BS) * 2
@@ -181,49 +187,35 @@ __device__ __forceinline__ void consume_tile(Tile& T, const u32x4 (&qb)[4], floa
   }
 }
 
-// One work item: chunk `split` of sequence b (length len > split*chunk) for
-// KV head kvh. All threads of the workgroup take part; the LDS buffers are
-// reused by the next item (the barrier after the id load separates them).
-template <int G, int BS, bool BF16>
-__device__ __forceinline__ void process_item(const AttnArgs& a, int b, int kvh, int split,
-                                             int len, int32_t* s_ids, float (*s_o)[G][kD],
-                                             float (*s_m)[G], float (*s_l)[G]) {
+template <int G>
+struct Smem {
+  int32_t ids[kMaxIds];
+  __attribute__((aligned(16))) float o[kWaves][G][kD];
+  float m[kWaves][G];
+  float l[kWaves][G];
+};
+
+// Attends tiles [j0, j1) of (sequence b, KV head kvh) with all four waves
+// (wave w takes tiles j0 + w, j0 + w + 4, ...; two tiles in flight) and hands
+// the merged (max, sum, unnormalised output) of each (head g, channel d) to
+// emit(), with the (g, d) pairs spread over the workgroup's threads.
+template <int G, int BS, bool BF16, typename Emit>
+__device__ __forceinline__ void attend_segment(const AttnArgs& a, int b, int kvh, int len, int j0,
+                                               int j1, Smem<G>& sm, Emit&& emit) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int r16 = lane & 15;
   const int q4 = lane >> 4;
-  const int Hq = a.q_heads;
-  const int chunk = a.chunk;
-  const int n_split_b = (len + chunk - 1) / chunk;
-  const int c_start = split * chunk;
-  const int nvalid = min(chunk, len - c_start);
-  const int nb = chunk / BS;
-
-  // Block ids of the chunk and q are loaded together (one memory round trip).
-  if (tid < nb) {
-    const int j = c_start / BS + tid;
-    int id = -1;
-    if (j * BS < len) {
-      id = a.table[int64_t(b) * a.max_blocks + j];
-      if (id < 0 || id >= a.n_local) {
-        atomicAdd(a.err_count, 1);
-        id = -1;
-      }
-    }
-    s_ids[tid] = id;
-  }
   // Q^T as the B operand: lane (head r16, q4) holds channels 32kk + 8q4 .. +8.
   u32x4 qb[4];
   {
     const char* qrow = reinterpret_cast<const char*>(a.q) +
-                       (int64_t(b) * Hq + kvh * G + r16) * kD * 2 + q4 * 16;
+                       (int64_t(b) * a.q_heads + kvh * G + r16) * kD * 2 + q4 * 16;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk)
       qb[kk] = r16 < G ? ld16(qrow + kk * 64) : u32x4{0, 0, 0, 0};
   }
-  __syncthreads();
-
   const char* pool = a.local;
   const int64_t Bb = a.block_bytes;
   float m = -INFINITY;   // running max of this lane's head (log2 domain)
@@ -232,23 +224,40 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, int b, int kvh, 
 #pragma unroll
   for (int n = 0; n < 8; ++n) o[n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
-  // Iterations of this wave that hold valid tokens; loads run one ahead.
-  const int its = chunk / (kWaves * kIt);
-  const int w0 = wave * its * kIt;
-  const int n_it = nvalid <= w0 ? 0 : min(its, (nvalid - w0 + kIt - 1) / kIt);
-  Tile A, B;
-  auto load_at = [&](Tile& T, int it) {
-    load_tile<BS>(T, w0 + it * kIt, nvalid, s_ids, pool, Bb, kvh, r16, q4);
-  };
-  if (n_it > 0) load_at(A, 0);
-  for (int it = 0; it < n_it; it += 2) {
-    consume_tile<BF16>(A, qb, a.scale_log2, m, lsum, o, [&] {
-      if (it + 1 < n_it) load_at(B, it + 1);
-    });
-    if (it + 1 >= n_it) break;
-    consume_tile<BF16>(B, qb, a.scale_log2, m, lsum, o, [&] {
-      if (it + 2 < n_it) load_at(A, it + 2);
-    });
+  for (int p0 = j0; p0 < j1; p0 += kPieceTiles) {
+    const int p1 = min(j1, p0 + kPieceTiles);
+    const int blk0 = p0 * kIt / BS;
+    const int cnt = (p1 * kIt - 1) / BS - blk0 + 1;
+    __syncthreads();                      // the previous piece's ids are no longer read
+    if (tid < cnt) {
+      const int j = blk0 + tid;
+      int id = -1;
+      if (j * BS < len) {
+        id = a.table[int64_t(b) * a.max_blocks + j];
+        if (id < 0 || id >= a.n_local) {
+          atomicAdd(a.err_count, 1);
+          id = -1;
+        }
+      }
+      sm.ids[tid] = id;
+    }
+    __syncthreads();
+    const int nt = p1 - p0;
+    const int n_it = nt > wave ? (nt - wave + kWaves - 1) / kWaves : 0;
+    auto load_at = [&](Tile& T, int k) {
+      load_tile<BS>(T, (p0 + wave + k * kWaves) * kIt, len, blk0, sm.ids, pool, Bb, kvh, r16, q4);
+    };
+    Tile A, B;
+    if (n_it > 0) load_at(A, 0);
+    for (int it = 0; it < n_it; it += 2) {
+      consume_tile<BF16>(A, qb, a.scale_log2, m, lsum, o, [&] {
+        if (it + 1 < n_it) load_at(B, it + 1);
+      });
+      if (it + 1 >= n_it) break;
+      consume_tile<BF16>(B, qb, a.scale_log2, m, lsum, o, [&] {
+        if (it + 2 < n_it) load_at(A, it + 2);
+      });
+    }
   }
 
   // ---- merge the four waves ------------------------------------------------
@@ -256,61 +265,53 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, int b, int kvh, 
   lsum += __shfl_xor(lsum, 32);
   if (r16 < G) {
     if (q4 == 0) {
-      s_m[wave][r16] = m;
-      s_l[wave][r16] = lsum;
+      sm.m[wave][r16] = m;
+      sm.l[wave][r16] = lsum;
     }
 #pragma unroll
     for (int n = 0; n < 8; ++n)
-      *reinterpret_cast<f32x4*>(&s_o[wave][r16][16 * n + 4 * q4]) = o[n];
+      *reinterpret_cast<f32x4*>(&sm.o[wave][r16][16 * n + 4 * q4]) = o[n];
   }
   __syncthreads();
-  const bool single = n_split_b == 1;
   for (int e = tid; e < G * kD; e += kThreads) {
     const int g = e / kD;
     const int d = e % kD;
     float M = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][g]);
+    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sm.m[w][g]);
     float L = 0.0f, O = 0.0f;
     if (M != -INFINITY) {
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) {
-        const float mw = s_m[w][g];
+        const float mw = sm.m[w][g];
         if (mw == -INFINITY) continue;
         const float f = exp2f(mw - M);
-        L = fmaf(f, s_l[w][g], L);
-        O = fmaf(f, s_o[w][g][d], O);
+        L = fmaf(f, sm.l[w][g], L);
+        O = fmaf(f, sm.o[w][g][d], O);
       }
     }
-    const int hq = kvh * G + g;
-    if (single) {
-      a.out[(int64_t(b) * Hq + hq) * kD + d] = L > 0.0f ? O / L : 0.0f;
-    } else {
-      const int64_t row = (int64_t(b) * Hq + hq) * a.n_split + split;
-      a.part_o[row * kD + d] = O;
-      if (d == 0) {
-        a.part_ml[row * 2] = M;
-        a.part_ml[row * 2 + 1] = L;
-      }
-    }
+    emit(g, d, M, L, O);
   }
 }
+
+// Workgroup-uniform value kept in a scalar register.
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 __device__ __forceinline__ void write_zeros(const AttnArgs& a, int b) {
   for (int e = threadIdx.x; e < a.q_heads * kD; e += kThreads)
     a.out[int64_t(b) * a.q_heads * kD + e] = 0.0f;
 }
 
-// Persistent form: gridDim.x workgroups (as many as stay resident) share the
-// work list. Each reads every sequence length once, counts its chunks,
-// prefix-sums the counts in LDS and then takes items blockIdx.x,
-// blockIdx.x + gridDim.x, ... ; item i -> (sequence, chunk, KV head) with the
-// KV head fastest. No workgroup is launched only to find it has no work.
+// Stream-K form. Every workgroup reads all lengths once and prefix-sums the
+// tile counts n_t(b) * Hkv in LDS; units are ordered (sequence, KV head,
+// tile) and workgroup w takes units [w*per, (w+1)*per), per = ceil(U/grid).
+// For each (sequence, KV head) it touches, it writes the output directly when
+// it holds all of that pair's tiles, else a partial into slot 2w (its first
+// pair) or 2w+1 (its last pair). The workgroup that holds a pair's first tile
+// records (first workgroup, last workgroup, its slot) for the combine.
 template <int G, int BS, bool BF16>
-__global__ __launch_bounds__(kThreads, 2) void attn_mfma_persistent(AttnArgs a) {
-  __shared__ int32_t s_ids[kMaxIds];
-  __shared__ __attribute__((aligned(16))) float s_o[kWaves][G][kD];
-  __shared__ float s_m[kWaves][G], s_l[kWaves][G];
+__global__ __launch_bounds__(kThreads, 2) void attn_mfma_streamk(AttnArgs a) {
+  __shared__ Smem<G> sm;
   __shared__ int32_t s_len[kMaxPersistBatch];
   __shared__ int32_t s_pref[kMaxPersistBatch + 1];
   __shared__ int32_t s_seg[kThreads];
@@ -318,10 +319,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_persistent(AttnArgs a) 
   const int lane = tid & 63;
   const int B = a.batch;
   const int H = a.kv_heads;
-  const int chunk = a.chunk;
-  const int per = (B + kThreads - 1) / kThreads;
-  const int b0 = min(B, tid * per);
-  const int b1 = min(B, b0 + per);
+  const int per_t = (B + kThreads - 1) / kThreads;
+  const int b0 = min(B, tid * per_t);
+  const int b1 = min(B, b0 + per_t);
   int run = 0;
   for (int b = b0; b < b1; ++b) {
     const int raw = a.seq_lens[b];
@@ -329,11 +329,11 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_persistent(AttnArgs a) 
     if (blockIdx.x == 0 && len != raw && raw > 0) atomicAdd(a.err_count, 1);
     s_len[b] = len;
     s_pref[b] = run;
-    run += (len + chunk - 1) / chunk * H;
+    run += (len + kIt - 1) / kIt * H;
   }
   s_seg[tid] = run;
   __syncthreads();
-  if (tid < 64) {   // exclusive scan of the 256 segment totals
+  if (tid < 64) {   // exclusive scan of the 256 per-thread totals
     const int v0 = s_seg[4 * lane], v1 = s_seg[4 * lane + 1];
     const int v2 = s_seg[4 * lane + 2], v3 = s_seg[4 * lane + 3];
     int sum = v0 + v1 + v2 + v3;
@@ -352,28 +352,63 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_persistent(AttnArgs a) 
   __syncthreads();
   for (int b = b0; b < b1; ++b) s_pref[b] += s_seg[tid];
   __syncthreads();
-  for (int b = blockIdx.x; b < B; b += gridDim.x)
-    if (s_len[b] == 0) write_zeros(a, b);
-  const int total = s_pref[B];
-  for (int item = blockIdx.x; item < total; item += gridDim.x) {
-    int lo = 0, hi = B - 1;   // last sequence whose first item is <= item
+  for (int b = blockIdx.x; b < B; b += gridDim.x) {
+    if (s_len[b] != 0) continue;
+    write_zeros(a, b);
+    for (int h = tid; h < H; h += kThreads) {
+      int32_t* info = a.info + (int64_t(b) * H + h) * 3;
+      info[0] = info[1] = info[2] = 0;
+    }
+  }
+
+  const int U = s_pref[B];
+  const int per = (U + int(gridDim.x) - 1) / int(gridDim.x);
+  int u = min(U, int(blockIdx.x) * per);
+  const int u_end = min(U, u + per);
+  for (int seg = 0; u < u_end; ++seg) {
+    int lo = 0, hi = B - 1;   // last sequence whose first unit is <= u
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
-      if (s_pref[mid] <= item) lo = mid;
+      if (s_pref[mid] <= u) lo = mid;
       else hi = mid - 1;
     }
-    const int r = item - s_pref[lo];
-    process_item<G, BS, BF16>(a, lo, r % H, r / H, s_len[lo], s_ids, s_o, s_m, s_l);
+    const int b = uniform(lo);
+    const int len = uniform(s_len[b]);
+    const int nt = (len + kIt - 1) / kIt;
+    const int r = u - uniform(s_pref[b]);
+    const int kvh = r / nt;
+    const int j0 = r - kvh * nt;
+    const int j1 = min(nt, j0 + (u_end - u));
+    const bool whole = j0 == 0 && j1 == nt;
+    const int64_t slot = int64_t(blockIdx.x) * 2 + (seg == 0 ? 0 : 1);
+    attend_segment<G, BS, BF16>(a, b, kvh, len, j0, j1, sm,
+                                [&](int g, int d, float M, float L, float O) {
+      if (whole) {
+        a.out[(int64_t(b) * a.q_heads + kvh * G + g) * kD + d] = L > 0.0f ? O / L : 0.0f;
+      } else {
+        a.part_o[(slot * G + g) * kD + d] = O;
+        if (d == 0) {
+          a.part_ml[(slot * G + g) * 2] = M;
+          a.part_ml[(slot * G + g) * 2 + 1] = L;
+        }
+      }
+    });
+    if (j0 == 0 && tid == 0) {
+      int32_t* info = a.info + (int64_t(b) * H + kvh) * 3;
+      info[0] = int(blockIdx.x);
+      info[1] = (uniform(s_pref[b]) + kvh * nt + nt - 1) / per;
+      info[2] = seg == 0 ? 0 : 1;
+    }
+    u += j1 - j0;
   }
 }
 
-// Grid form for batches too large for the persistent work list:
-// grid (chunk, KV head, sequence); workgroups past a sequence's end exit.
+// Grid form for batches too large for the LDS work list: grid (chunk of
+// kGridChunkTiles tiles, KV head, sequence); partials go to row
+// (sequence, query head, chunk) and the split-K combine merges them.
 template <int G, int BS, bool BF16>
 __global__ __launch_bounds__(kThreads, 2) void attn_mfma_grid(AttnArgs a) {
-  __shared__ int32_t s_ids[kMaxIds];
-  __shared__ __attribute__((aligned(16))) float s_o[kWaves][G][kD];
-  __shared__ float s_m[kWaves][G], s_l[kWaves][G];
+  __shared__ Smem<G> sm;
   const int split = blockIdx.x;
   const int kvh = blockIdx.y;
   const int b = blockIdx.z;
@@ -385,8 +420,85 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_grid(AttnArgs a) {
     if (split == 0 && kvh == 0) write_zeros(a, b);
     return;
   }
-  if (split >= (len + a.chunk - 1) / a.chunk) return;
-  process_item<G, BS, BF16>(a, b, kvh, split, len, s_ids, s_o, s_m, s_l);
+  const int nt = (len + kIt - 1) / kIt;
+  const int j0 = split * kGridChunkTiles;
+  if (j0 >= nt) return;
+  const int j1 = min(nt, j0 + kGridChunkTiles);
+  attend_segment<G, BS, BF16>(a, b, kvh, len, j0, j1, sm,
+                              [&](int g, int d, float M, float L, float O) {
+    const int hq = kvh * G + g;
+    if (j0 == 0 && j1 == nt) {
+      a.out[(int64_t(b) * a.q_heads + hq) * kD + d] = L > 0.0f ? O / L : 0.0f;
+    } else {
+      const int64_t row = (int64_t(b) * a.q_heads + hq) * a.n_split + split;
+      a.part_o[row * kD + d] = O;
+      if (d == 0) {
+        a.part_ml[row * 2] = M;
+        a.part_ml[row * 2 + 1] = L;
+      }
+    }
+  });
+}
+
+// Online merge of partials [0, n) of one output; K loads of each kind per
+// memory round trip, branch-free (indices past n repeat the last partial and
+// are given weight 0), so all K loads are in flight together.
+template <int K>
+__device__ __forceinline__ void merge_partials(const AttnArgs& a, int G, int g, int d, int wa,
+                                               int sa, int n, float& M, float& L, float& O) {
+  for (int j0 = 0; j0 < n; j0 += K) {
+    float mm[K], ll[K], oo[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+      const int i = min(j0 + j, n - 1);
+      const int64_t slot = int64_t(wa + i) * 2 + (i == 0 ? sa : 0);
+      mm[j] = a.part_ml[(slot * G + g) * 2];
+      ll[j] = a.part_ml[(slot * G + g) * 2 + 1];
+      oo[j] = a.part_o[(slot * G + g) * kD + d];
+    }
+#pragma unroll
+    for (int j = 0; j < K; ++j)
+      if (j0 + j >= n) mm[j] = -INFINITY;
+    float Mb = M;
+#pragma unroll
+    for (int j = 0; j < K; ++j) Mb = fmaxf(Mb, mm[j]);
+    if (Mb == -INFINITY) continue;
+    const float f_old = M == -INFINITY ? 0.0f : exp2f(M - Mb);
+    L *= f_old;
+    O *= f_old;
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+      const float f = mm[j] == -INFINITY ? 0.0f : exp2f(mm[j] - Mb);
+      L = fmaf(f, ll[j], L);
+      O = fmaf(f, oo[j], O);
+    }
+    M = Mb;
+  }
+}
+
+// Merges the partials of every (sequence, KV head) the stream-K ranges cut.
+// Grid (pair, output group): each thread owns one (head, channel) output.
+// info says which workgroups hold the pair's partials (first == last: the
+// pair was written whole, or the sequence is empty).
+__global__ __launch_bounds__(kThreads) void attn_combine_streamk(AttnArgs a) {
+  const int H = a.kv_heads;
+  const int G = a.q_heads / H;
+  const int pair = blockIdx.x;
+  const int b = pair / H;
+  const int kvh = pair - b * H;
+  const int e = blockIdx.y * kThreads + threadIdx.x;
+  const int32_t* info = a.info + int64_t(pair) * 3;
+  const int wa = info[0], wb = info[1], sa = info[2];
+  if (wb <= wa || e >= G * kD) return;
+  const int g = e / kD;
+  const int d = e % kD;
+  const int n = wb - wa + 1;
+  float M = -INFINITY, L = 0.0f, O = 0.0f;
+  if (n <= 4)
+    merge_partials<4>(a, G, g, d, wa, sa, n, M, L, O);
+  else
+    merge_partials<16>(a, G, g, d, wa, sa, n, M, L, O);
+  a.out[(int64_t(b) * a.q_heads + kvh * G + g) * kD + d] = L > 0.0f ? O / L : 0.0f;
 }
 
 template <typename K>
@@ -401,18 +513,23 @@ int resident_workgroups(K kernel) {
 
 template <int G, int BS, bool BF16>
 hipError_t launch_typed(const AttnArgs& a, hipStream_t stream) {
-  if (a.batch <= kMaxPersistBatch) {
-    static const int resident = resident_workgroups(attn_mfma_persistent<G, BS, BF16>);
-    const int64_t upper = int64_t(a.batch) * a.kv_heads * a.n_split;
-    const int grid = int(std::max<int64_t>(1, std::min<int64_t>(resident > 0 ? resident : 512,
-                                                                 upper)));
-    hipLaunchKernelGGL((attn_mfma_persistent<G, BS, BF16>), dim3(grid), dim3(kThreads), 0,
-                       stream, a);
-  } else {
-    hipLaunchKernelGGL((attn_mfma_grid<G, BS, BF16>), dim3(a.n_split, a.kv_heads, a.batch),
-                       dim3(kThreads), 0, stream, a);
+  if (a.stream_k) {
+    static const int resident = resident_workgroups(attn_mfma_streamk<G, BS, BF16>);
+    const int grid = std::max(1, std::min(resident > 0 ? resident : 512, kMaxStreamGrid));
+    hipLaunchKernelGGL((attn_mfma_streamk<G, BS, BF16>), dim3(grid), dim3(kThreads), 0, stream,
+                       a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int groups = (a.q_heads / a.kv_heads * kD + kThreads - 1) / kThreads;
+    hipLaunchKernelGGL(attn_combine_streamk, dim3(a.batch * a.kv_heads, groups), dim3(kThreads),
+                       0, stream, a);
+    return hipGetLastError();
   }
-  return hipGetLastError();
+  hipLaunchKernelGGL((attn_mfma_grid<G, BS, BF16>), dim3(a.n_split, a.kv_heads, a.batch),
+                     dim3(kThreads), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.n_split <= 1) return e;
+  return launch_attn_combine(a, stream);
 }
 
 template <int G, int BS>
@@ -436,17 +553,14 @@ hipError_t launch_g(const AttnArgs& a, hipStream_t stream) {
 
 hipError_t launch_paged_attention_mfma(const AttnArgs& a, hipStream_t stream) {
   if (a.batch == 0) return hipSuccess;
-  hipError_t e;
   switch (a.q_heads / a.kv_heads) {
-    case 1: e = launch_g<1>(a, stream); break;
-    case 2: e = launch_g<2>(a, stream); break;
-    case 4: e = launch_g<4>(a, stream); break;
-    case 8: e = launch_g<8>(a, stream); break;
-    case 16: e = launch_g<16>(a, stream); break;
+    case 1: return launch_g<1>(a, stream);
+    case 2: return launch_g<2>(a, stream);
+    case 4: return launch_g<4>(a, stream);
+    case 8: return launch_g<8>(a, stream);
+    case 16: return launch_g<16>(a, stream);
     default: return hipErrorInvalidValue;
   }
-  if (e != hipSuccess || a.n_split <= 1) return e;
-  return launch_attn_combine(a, stream);
 }
 
 }  // namespace ema

@@ -24,14 +24,17 @@ def ema():
     return m
 
 
-@pytest.fixture(params=["mfma", "valu"])
+@pytest.fixture(params=["mfma", "mfma-grid", "valu"])
 def impl(request, monkeypatch):
-    """Attention kernel: the matrix-core one (default) or the vector-ALU one,
-    chosen when the slice is created."""
+    """Attention kernel and schedule, chosen when the slice is created: the
+    matrix-core kernel with stream-K scheduling (default), the matrix-core
+    grid form, or the vector-ALU kernel."""
+    monkeypatch.delenv("EMA_ATTN_KERNEL", raising=False)
+    monkeypatch.delenv("EMA_ATTN_SCHED", raising=False)
     if request.param == "valu":
         monkeypatch.setenv("EMA_ATTN_KERNEL", "valu")
-    else:
-        monkeypatch.delenv("EMA_ATTN_KERNEL", raising=False)
+    elif request.param == "mfma-grid":
+        monkeypatch.setenv("EMA_ATTN_SCHED", "grid")
     return request.param
 
 
@@ -145,6 +148,30 @@ def test_wide_batch_takes_the_long_chunk_path(ema, impl):
         assert ema.slice_device_errors(w.h) == 0
         got = out.cpu().numpy()
         assert np.all(got[0] == 0.0)
+        ref = oracle_attention(w, st, 0)
+        assert rel_err(got, ref) <= TOL, rel_err(got, ref)
+    finally:
+        w.close()
+
+
+@pytest.mark.parametrize("batch,hi,hkv,hq", [(600, 100, 2, 8), (2100, 40, 1, 4)])
+def test_many_short_sequences(ema, impl, batch, hi, hkv, hq):
+    """Stream-K ranges then cover several whole sequences each (written
+    directly) plus cut ones; above 2048 sequences the grid form takes over."""
+    print(f"short {impl} batch={batch}", flush=True)
+    rng = np.random.default_rng(batch)
+    lens = rng.integers(0, hi + 1, batch).tolist()
+    cfg = synth.KVConfig("short", 1, hq, hkv, 128, "f16", 16, batch, ("uniform", 0, 0), 0.4, 93)
+    w = Workload(cfg, lens=lens, staging_slots=1)
+    try:
+        st = w.oracle_mirror()
+        w.prefetch(0)
+        st.prefetch(w.pf_src[0], w.pf_dst[0])
+        out = w.new_out()
+        w.attention(0, out)
+        torch.cuda.synchronize()
+        assert ema.slice_device_errors(w.h) == 0
+        got = out.cpu().numpy()
         ref = oracle_attention(w, st, 0)
         assert rel_err(got, ref) <= TOL, rel_err(got, ref)
     finally:
