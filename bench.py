@@ -7,15 +7,28 @@ block 16, batch 64, lengths U[1024, 4096], 30 % of each layer's blocks in the
 slice). Per layer: the slice-resident blocks of layer l+1 are prefetched into a
 double-buffered staging area on one stream while paged decode attention of
 layer l runs on another (``--mode serial`` runs both on one stream: copy, then
-attention). After the timed steps the lender reclaims part of the slice a few
-times (compaction / write-back / preemption plus the device table rewrite).
+attention, the on-demand swap of the paper's ablation).
+
+After the timed steps, untimed by the step clock:
+  * symmetry: attention over every layer through the staged tables versus
+    through all-local tables holding the same tokens (each slice-resident block
+    migrated to a fresh local block), interleaved A B A B; the outputs of one
+    layer are compared bit for bit;
+  * cpu_baseline: the oracle on a bounded sample, on this host's cores (before
+    reclaim, which rewrites blocks the sample reads);
+  * reclaim: the lender takes part of the slice back a few times (compaction /
+    write-back / preemption plus the device table rewrite), timed on the device
+    behind a blocking copy so that host planning is not counted.
 
 Prints one JSON line. ``value`` is decode tokens/s of the whole step
 (batch / step time; attention only, no projections or MLP). The roofline
 object is for the attention entry point (its kernels' algorithmic HBM bytes
-over their mean duration, from HIP events on the attention stream).
+over their mean duration, from HIP events on the attention stream during the
+timed steps); its ``traffic`` comes from the committed counter summary of the
+same workload and is null when the kernel sources no longer match it.
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -29,6 +42,10 @@ for p in (ROOT, os.path.join(ROOT, "tests")):
         sys.path.insert(0, p)
 
 HBM_PEAK_GBPS = 8000.0
+# Sources whose code runs in one attention call; a counter record is valid for
+# the digest of exactly these files.
+ATTN_SOURCES = ("paper_2609_27040_amd/csrc/paged_attention_mfma.hip",
+                "paper_2609_27040_amd/csrc/kernels.h")
 
 
 def parse():
@@ -42,7 +59,13 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--reclaim-reps", type=int, default=4)
+    ap.add_argument("--symmetry-reps", type=int, default=6,
+                    help="A/B pairs of the staged vs all-local attention passes (0: skip)")
     return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
 def attention_bytes(w, layer=0):
@@ -53,6 +76,33 @@ def attention_bytes(w, layer=0):
     nblk = int(((w.lens + w.bs - 1) // w.bs).sum())
     hq = w.cfg.q_heads
     return (toks * 2 * w.hkv * w.D * e + w.B * hq * w.D * (e + 4) + 4 * nblk + 4 * w.B)
+
+
+def sources_digest():
+    h = hashlib.sha256()
+    for rel in ATTN_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(workload):
+    """HBM bytes per attention call from the committed counter summary, or None
+    when there is none or it was taken on other kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"paged_attention_{workload}_counters.md")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        for line in f:
+            if line.startswith("traffic-record:"):
+                rec = json.loads(line.split(":", 1)[1])
+                if rec.get("sources") == sources_digest():
+                    return rec
+    return None
+
+
+def pct(a, q):
+    return float(np.percentile(np.asarray(a), q))
 
 
 def cpu_baseline(w, seconds):
@@ -98,8 +148,95 @@ def cpu_baseline(w, seconds):
             "host_cores_available": len(os.sched_getaffinity(0))}
 
 
-def log(msg):
-    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+def symmetry(w, out, s, reps, ema, torch):
+    """Staged versus all-local attention tables over the same tokens.
+
+    Every slice-resident block of every layer is migrated to a fresh local
+    block (allocated in a seeded random order, so ids are as scattered as the
+    canonical local ones). Pass A runs attention over all layers through the
+    staged tables, pass B through the all-local tables; passes alternate.
+    Layer 0 is prefetched first and its two outputs must match bit for bit.
+    The fresh blocks are freed again at the end."""
+    L = w.L
+    sl = w.tables >= w.n_local
+    src = w.tables[sl].astype(np.int32)
+    owners = np.nonzero(sl)[1]
+    perm = np.random.default_rng(w.cfg.seed + 1).permutation(len(src))
+    fresh = ema.slice_alloc_blocks(w.h, ema.POOL_LOCAL, owners[perm])
+    dst = np.empty(len(src), dtype=np.int32)
+    dst[perm] = fresh
+    i32 = lambda a: torch.as_tensor(np.ascontiguousarray(a, dtype=np.int32), device="cuda")
+    ema.slice_migrate(w.h, i32(src), i32(dst), stream=s)
+    local_tabs = w.tables.copy()
+    local_tabs[sl] = dst
+    local_dev = i32(local_tabs)
+    # bitwise check on layer 0
+    w.prefetch(0, stream=s)
+    out_b = w.new_out()
+    w.attention(0, out, stream=s)
+    w.attention(0, out_b, table=local_dev[0], stream=s)
+    torch.cuda.synchronize()
+    identical = bool(torch.equal(out, out_b))
+
+    def run(tabs):
+        for l in range(L):
+            w.attention(l, out, table=tabs[l], stream=s)
+
+    run(w.attn_dev)
+    run(local_dev)
+    ms = {"staged": [], "local": []}
+    for _ in range(reps):
+        for kind, tabs in (("staged", w.attn_dev), ("local", local_dev)):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            run(tabs)
+            e1.record(s)
+            e1.synchronize()
+            ms[kind].append(e0.elapsed_time(e1))
+    torch.cuda.synchronize()
+    ema.slice_free_blocks(w.h, fresh)
+    med = {k: float(np.median(v)) for k, v in ms.items()}
+    return {"outputs_identical": identical,
+            "staged_ms_per_step": med["staged"], "local_ms_per_step": med["local"],
+            "staged_p10_p90": [pct(ms["staged"], 10), pct(ms["staged"], 90)],
+            "local_p10_p90": [pct(ms["local"], 10), pct(ms["local"], 90)],
+            "ratio": med["staged"] / med["local"],
+            "attention_us_per_layer": med["staged"] * 1e3 / L,
+            "reps": reps, "moved_blocks": int(len(src))}
+
+
+def reclaim_phase(w, s, reps, ema, torch):
+    """The lender takes 5 % of its lent blocks back, ``reps`` times. Each call is
+    queued behind a 2 GiB device copy so that the events bracket only device work
+    (upload of the plan, block copies, table rewrite); ``host_plan_ms`` is the
+    call's host time."""
+    blk_a = torch.empty(1 << 30, dtype=torch.int16, device="cuda")
+    blk_b = torch.empty_like(blk_a)
+    # one untimed call sizes the library's work buffers
+    ema.slice_reclaim(w.h, 1, w.tables_dev.view(-1), stream=s)
+    ema.slice_lend(w.h, 1)
+    torch.cuda.synchronize()
+    res = []
+    for _ in range(reps):
+        lim = ema.slice_get_info(w.h)["lim"]
+        n = max(1, lim // 20)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(s):
+            blk_b.copy_(blk_a)
+        e0.record(s)
+        c0 = time.perf_counter()
+        r = ema.slice_reclaim(w.h, n, w.tables_dev.view(-1), stream=s)
+        c1 = time.perf_counter()
+        covered = not e0.query()      # the blocker was still running when the call returned
+        e1.record(s)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        nbytes = 2 * r["moved"] * w.bb + 8 * w.tables_dev.numel()
+        res.append({"n": n, "moved": r["moved"], "written_back": r["written_back"],
+                    "victims": len(r["victims"]), "ms": ms, "host_plan_ms": (c1 - c0) * 1e3,
+                    "device_only": covered, "GBps": nbytes / (ms / 1e3) / 1e9})
+    del blk_a, blk_b
+    return res
 
 
 def main():
@@ -119,7 +256,11 @@ def main():
     torch.cuda.set_device(0)
     cfg = synth.CONFIGS[args.workload]
     log(f"setting up {cfg.name}")
-    w = Workload(cfg, fill="device")
+    probe = synth.placement(cfg, synth.seq_lens(cfg, np.random.default_rng(cfg.seed)),
+                            np.random.default_rng(cfg.seed))
+    extra = len(probe.slice_order) if args.symmetry_reps > 0 else 0
+    del probe
+    w = Workload(cfg, fill="device", extra_local=extra)
     L, B = w.L, w.B
     log(f"{L} layers, batch {B}, {w.n_local} local + {w.slice_view.shape[0]} slice blocks")
     s1 = torch.cuda.Stream()
@@ -189,26 +330,12 @@ def main():
     attn_gbps = attn_b / at_mean_s / 1e9
     pf_gbps = float(np.sum(pf_b) * args.steps / (pf_ms.sum() / 1e3) / 1e9)
     step_bytes = attn_b * L + float(np.sum(pf_b))
+    log(f"{ms_step:.3f} ms/step, attention {at_mean_s * 1e6:.1f} us/layer")
 
-    log(f"{ms_step:.3f} ms/step; reclaim")
-    # ---- reclaim: the lender takes part of the slice back, a few times ----------------
-    reclaim = []
-    for _ in range(args.reclaim_reps):
-        lim = ema.slice_get_info(w.h)["lim"]
-        n = max(1, lim // 20)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        e0.record(s1)
-        c0 = time.perf_counter()
-        r = ema.slice_reclaim(w.h, n, w.tables_dev.view(-1), stream=s1)
-        c1 = time.perf_counter()
-        e1.record(s1)
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1)
-        nbytes = 2 * r["moved"] * w.bb + 8 * w.tables_dev.numel()
-        reclaim.append({"n": n, "moved": r["moved"], "written_back": r["written_back"],
-                        "victims": len(r["victims"]), "ms": ms, "host_plan_ms": (c1 - c0) * 1e3,
-                        "GBps": nbytes / (ms / 1e3) / 1e9})
+    traffic = None
+    rec = counter_traffic(cfg.name)
+    if rec is not None:
+        traffic = rec["bytes_per_call"]
 
     res = {
         "metric": "prefetch/reclaim GB/s + paged decode tokens/s, % of HBM roofline, 1 GPU",
@@ -228,18 +355,36 @@ def main():
                    "block_size": cfg.block_size, "lens": list(cfg.lens),
                    "slice_frac": cfg.slice_frac, "mode": args.mode},
         "roofline": {"bound": "hbm", "achieved": attn_gbps, "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": attn_gbps / HBM_PEAK_GBPS, "traffic": None},
+                     "unit": "GB/s", "frac": attn_gbps / HBM_PEAK_GBPS, "traffic": traffic,
+                     "kernel": "paged_decode_attention (attn_mfma_streamk + attn_combine_streamk)"},
         "attention": {"bytes_per_launch": attn_b, "mean_us": at_mean_s * 1e6,
+                      "p10_us": pct(at_ms, 10) * 1e3, "p90_us": pct(at_ms, 90) * 1e3,
                       "GBps": attn_gbps, "frac": attn_gbps / HBM_PEAK_GBPS},
         "prefetch": {"bytes_per_step": float(np.sum(pf_b)), "mean_us": float(pf_ms.mean()) * 1e3,
                      "GBps": pf_gbps, "frac": pf_gbps / HBM_PEAK_GBPS},
         "step": {"bytes": step_bytes, "GBps": step_bytes / (ms_step / 1e3) / 1e9,
                  "frac": step_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBPS},
-        "reclaim": reclaim,
     }
+    if rec is not None:
+        res["roofline"]["traffic_source"] = rec.get("note", "counter summary")
+
+    if args.symmetry_reps > 0:
+        log("symmetry: staged vs all-local tables")
+        sym = symmetry(w, out, s1, args.symmetry_reps, ema, torch)
+        sym["step_vs_all_local_attention"] = ms_step / sym["local_ms_per_step"]
+        res["symmetry"] = sym
+        iso = attn_b / (sym["attention_us_per_layer"] / 1e6) / 1e9
+        res["attention"]["isolated_GBps"] = iso
+        res["attention"]["isolated_frac"] = iso / HBM_PEAK_GBPS
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    if args.reclaim_reps > 0:
+        log("reclaim")
+        res["reclaim"] = reclaim_phase(w, s1, args.reclaim_reps, ema, torch)
+    errs = ema.slice_device_errors(w.h)
+    if errs:
+        raise RuntimeError(f"kernels skipped {errs} invalid ids")
     w.close()
     print(json.dumps(res))
 
