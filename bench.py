@@ -207,15 +207,22 @@ def symmetry(w, out, s, reps, ema, torch):
 
 def reclaim_phase(w, s, reps, ema, torch):
     """The lender takes 5 % of its lent blocks back, ``reps`` times. Each call is
-    queued behind a 2 GiB device copy so that the events bracket only device work
-    (upload of the plan, block copies, table rewrite); ``host_plan_ms`` is the
-    call's host time."""
-    blk_a = torch.empty(1 << 30, dtype=torch.int16, device="cuda")
-    blk_b = torch.empty_like(blk_a)
-    # one untimed call sizes the library's work buffers
-    ema.slice_reclaim(w.h, 1, w.tables_dev.view(-1), stream=s)
-    ema.slice_lend(w.h, 1)
+    queued behind a device copy long enough to outlast the call's host planning
+    (sized from an untimed call of the same size, whose slots are lent back), so
+    that the events bracket only device work: upload of the plan, block copies,
+    table rewrite. ``host_plan_ms`` is the call's host time; ``device_only`` says
+    whether the copy was indeed still running when the call returned."""
+    lim = ema.slice_get_info(w.h)["lim"]
+    n0 = max(1, lim // 20)
+    c0 = time.perf_counter()
+    ema.slice_reclaim(w.h, n0, w.tables_dev.view(-1), stream=s)
+    host_s = time.perf_counter() - c0
+    ema.slice_lend(w.h, n0)
     torch.cuda.synchronize()
+    # about 5 TB/s of copy traffic: 3x the host time, at least 2 GiB, at most 32 GiB
+    nbytes = int(min(32 << 30, max(2 << 30, 3 * host_s * 5e12 / 2)))
+    blk_a = torch.empty(nbytes // 2, dtype=torch.int16, device="cuda")
+    blk_b = torch.empty_like(blk_a)
     res = []
     for _ in range(reps):
         lim = ema.slice_get_info(w.h)["lim"]
@@ -231,10 +238,10 @@ def reclaim_phase(w, s, reps, ema, torch):
         e1.record(s)
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1)
-        nbytes = 2 * r["moved"] * w.bb + 8 * w.tables_dev.numel()
+        nb = 2 * r["moved"] * w.bb + 8 * w.tables_dev.numel()
         res.append({"n": n, "moved": r["moved"], "written_back": r["written_back"],
                     "victims": len(r["victims"]), "ms": ms, "host_plan_ms": (c1 - c0) * 1e3,
-                    "device_only": covered, "GBps": nbytes / (ms / 1e3) / 1e9})
+                    "device_only": covered, "GBps": nb / (ms / 1e3) / 1e9})
     del blk_a, blk_b
     return res
 

@@ -20,10 +20,15 @@ constexpr int kUnitBytes = 4096;
 constexpr int kWaves = 4;
 constexpr int kTileRow = 128 + 8;   // u16 per LDS tile row (padded, keeps 16 B alignment)
 
+// Block data is touched once per copy: streaming (non-temporal) loads and
+// stores keep it from displacing other data in L2 and the memory-side cache,
+// and keep written lines from being flushed later under another kernel's reads.
 __device__ __forceinline__ u32x4 ld16(const char* p) {
-  return *reinterpret_cast<const u32x4*>(p);
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
 }
-__device__ __forceinline__ void st16(char* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+__device__ __forceinline__ void st16(char* p, u32x4 v) {
+  __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+}
 
 // LDS writes of this wave must land before other lanes of the wave read them.
 __device__ __forceinline__ void wave_lds_sync() {

@@ -53,6 +53,11 @@ constexpr int kGridChunkTiles = 32;        // tiles per workgroup in the grid fa
 __device__ __forceinline__ u32x4 ld16(const char* p) {
   return *reinterpret_cast<const u32x4*>(p);
 }
+// K/V are read exactly once per call: streaming loads keep them from
+// displacing tables, queries and partials in L2 and the memory-side cache.
+__device__ __forceinline__ u32x4 ld16_stream(const char* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
 
 template <bool BF16>
 __device__ __forceinline__ f32x4 mfma(u32x4 a, u32x4 b, f32x4 c) {
@@ -113,7 +118,7 @@ __device__ __forceinline__ void load_tile(Tile& T, int t0, int len, int blk0, co
     const char* p = pool + (ok ? int64_t(id) * Bb + (int64_t(kvh * BS + tok % BS) * kD + q4 * 8) * 2
                                : int64_t(0));
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) T.k[t][kk] = ld16(p + kk * 64);
+    for (int kk = 0; kk < 4; ++kk) T.k[t][kk] = ld16_stream(p + kk * 64);
   }
   // V^T rows: d-tile n, row 16n + r16, tokens t0 + 8q4 .. +8 (one block).
   const int vt = t0 + 8 * q4;
@@ -124,7 +129,7 @@ __device__ __forceinline__ void load_tile(Tile& T, int t0, int len, int blk0, co
                                          (int64_t(kvh * kD + r16) * BS + vt % BS) * 2
                                    : int64_t(0));
 #pragma unroll
-  for (int n = 0; n < 8; ++n) T.v[n] = ld16(p + int64_t(16 * n) * BS * 2);
+  for (int n = 0; n < 8; ++n) T.v[n] = ld16_stream(p + int64_t(16 * n) * BS * 2);
 }
 
 // Scores, online softmax update and P.V for one loaded iteration.
