@@ -54,7 +54,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama3-8b-kv",
-                    choices=["llama3-8b-kv", "llama-70b-tp8-share"])
+                    choices=["llama3-8b-kv", "llama-70b-tp8-share", "bursty-8b"])
     ap.add_argument("--mode", default="overlap", choices=["overlap", "serial"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
@@ -246,6 +246,64 @@ def reclaim_phase(w, s, reps, ema, torch):
     return res
 
 
+def bursty_main(args):
+    """The bursty elastic trace: every step the lender lends or reclaims 1-25 %
+    of the slice, the borrower's slice fraction takes a random-walk step and
+    blocks migrate, then one overlapped decode step runs; prints the per-step
+    latency distribution (one JSON line)."""
+    import torch
+    import synth
+    from bursty import BurstyTrace
+
+    torch.cuda.set_device(0)
+    cfg = synth.BURSTY
+    log("setting up bursty-8b")
+    tr = BurstyTrace(cfg, fill="device")
+    w = tr.w
+    steps = cfg.extra["steps"]
+    recs, gbps = [], []
+    for k in range(steps):
+        rec = tr.step()
+        tr.check_invariants()
+        pf = sum(2 * len(s) * w.bb for s in w.pf_src)
+        toks = int(w.lens.sum())
+        attn = w.L * (toks * 2 * w.hkv * w.D * 2)
+        gbps.append((attn + pf) / (rec["ms"] / 1e3) / 1e9)
+        recs.append(rec)
+        if (k + 1) % 50 == 0:
+            log(f"step {k + 1}: {rec['ms']:.3f} ms, slice fraction {rec['slice_frac']:.2f}")
+    from paper_2609_27040_amd import ema
+    errs = ema.slice_device_errors(w.h)
+    if errs:
+        raise RuntimeError(f"kernels skipped {errs} invalid ids")
+    ms = np.array([r["ms"] for r in recs])
+    fr = np.array([r["slice_frac"] for r in recs])
+    res = {
+        "metric": "prefetch/reclaim GB/s + paged decode tokens/s, % of HBM roofline, 1 GPU",
+        "value": w.B / (float(np.median(ms)) / 1e3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": steps, "warmup": 0,
+        "ms_per_step": float(np.median(ms)),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": cfg.dtype, "data": "synthetic",
+        "config": {"workload": cfg.name, "layers": w.L, "batch": w.B, "q_heads": cfg.q_heads,
+                   "kv_heads": cfg.kv_heads, "head_dim": cfg.head_dim,
+                   "block_size": cfg.block_size, "lens": list(cfg.lens),
+                   "frac_max": cfg.extra["frac_max"], "step_frac": list(cfg.extra["step_frac"])},
+        "step_ms": {"p10": pct(ms, 10), "p50": pct(ms, 50), "p90": pct(ms, 90),
+                    "max": float(ms.max())},
+        "step_GBps": {"p10": pct(gbps, 10), "p50": pct(gbps, 50), "p90": pct(gbps, 90)},
+        "slice_frac": {"min": float(fr.min()), "max": float(fr.max())},
+        "lender": {"reclaims": sum(1 for e in tr.log if e[0] == "reclaim"),
+                   "lends": sum(1 for e in tr.log if e[0] == "lend"),
+                   "moved_blocks": int(sum(e[2] for e in tr.log if e[0] == "reclaim")),
+                   "preempted": int(sum(len(e[4]) for e in tr.log if e[0] == "reclaim"))},
+        "migrated_blocks": int(sum(e[2] for e in tr.log if e[0] == "migrate")),
+    }
+    tr.close()
+    print(json.dumps(res))
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -255,9 +313,12 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
+    if args.workload == "bursty-8b":
+        bursty_main(args)
+        return
     import torch
     import synth
-    from harness import Workload
+    from harness import StepRunner, Workload
     from paper_2609_27040_amd import ema
 
     torch.cuda.set_device(0)
@@ -270,58 +331,21 @@ def main():
     w = Workload(cfg, fill="device", extra_local=extra)
     L, B = w.L, w.B
     log(f"{L} layers, batch {B}, {w.n_local} local + {w.slice_view.shape[0]} slice blocks")
-    s1 = torch.cuda.Stream()
-    s2 = torch.cuda.Stream() if args.mode == "overlap" else s1
+    runner = StepRunner(w, args.mode)
+    s1 = runner.s1
     out = w.new_out()
     attn_b = attention_bytes(w)
     pf_b = [2 * len(w.pf_src[l]) * w.bb for l in range(L)]
 
-    ev_pf = [torch.cuda.Event() for _ in range(L)]
-    ev_at = [torch.cuda.Event() for _ in range(L)]
-
-    def step(timers):
-        for l in range(L):
-            if l == 0:
-                # staging slots 0/1 were last read by the previous step's last layers
-                s2.wait_event(ev_at[L - 1])
-                if L >= 2:
-                    s2.wait_event(ev_at[L - 2])
-                if timers:
-                    timers["pf"][0][0].record(s2)
-                w.prefetch(0, stream=s2)
-                if timers:
-                    timers["pf"][0][1].record(s2)
-                ev_pf[0].record(s2)
-            if l + 1 < L:
-                if l >= 1:
-                    s2.wait_event(ev_at[l - 1])   # slot (l+1) % 2 was read by layer l-1
-                if timers:
-                    timers["pf"][l + 1][0].record(s2)
-                w.prefetch(l + 1, stream=s2)
-                if timers:
-                    timers["pf"][l + 1][1].record(s2)
-                ev_pf[l + 1].record(s2)
-            s1.wait_event(ev_pf[l])
-            if timers:
-                timers["at"][l][0].record(s1)
-            w.attention(l, out, stream=s1)
-            if timers:
-                timers["at"][l][1].record(s1)
-            ev_at[l].record(s1)
-
-    def new_timers():
-        mk = lambda: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-        return {"pf": [mk() for _ in range(L)], "at": [mk() for _ in range(L)]}
-
     log(f"warmup {args.warmup}, timed {args.steps} steps ({args.mode})")
     for _ in range(args.warmup):
-        step(None)
+        runner.run(out)
     torch.cuda.synchronize()
-    timers = [new_timers() for _ in range(args.steps)]
+    timers = [runner.new_timers() for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
-        step(timers[k])
+        runner.run(out, timers[k])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps

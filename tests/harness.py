@@ -25,7 +25,7 @@ TORCH_DT = {"f16": torch.float16, "bf16": torch.bfloat16}
 class Workload:
     def __init__(self, cfg, layers=None, batch=None, slice_layout=ema.LAYOUT_ATTN, seed=None,
                  staging_slots=2, extra_local=0, extra_slice=0, fill="host", checked=False,
-                 lens=None, frac=None, shuffle=True):
+                 lens=None, frac=None, shuffle=True, stage_n=None):
         self.cfg = cfg = cfg if batch is None else cfg.scaled(batch=batch)
         self.L = cfg.layers if layers is None else layers
         rng = np.random.default_rng(cfg.seed if seed is None else seed)
@@ -38,7 +38,8 @@ class Workload:
         self.maxblk = max(pl.maxblk, 1)
         self.slice_layout = slice_layout
         self.slice_per_layer = pl.in_slice.reshape(self.L, -1).sum(axis=1)
-        self.stage_n = int(self.slice_per_layer.max()) if self.L else 0
+        self.stage_n = (int(self.slice_per_layer.max()) if self.L else 0) if stage_n is None \
+            else int(stage_n)
         self.staging_slots = staging_slots
         n_local = len(pl.local_order) + staging_slots * self.stage_n + extra_local
         n_slice = len(pl.slice_order) + extra_slice
@@ -59,25 +60,13 @@ class Workload:
         self.alloc_log.append((ema.POOL_LOCAL, st_owners))
         info = ema.slice_get_info(self.h)
         self.n_local = info["n_local"]
-        # per-layer prefetch lists and attention tables
-        self.pf_src, self.pf_dst = [], []
-        attn = tables.copy()
-        for l in range(self.L):
-            mask = tables[l] >= self.n_local
-            src = tables[l][mask]
-            dst = self.staging[l % staging_slots, :len(src)]
-            attn[l][mask] = dst
-            self.pf_src.append(src.astype(np.int32))
-            self.pf_dst.append(dst.astype(np.int32))
-        self.attn_tables = attn
         self.q16 = synth.q_values(cfg, rng, self.B)
         dev = torch.device("cuda")
         self.q = torch.from_numpy(self.q16.view(np.int16)).to(dev).view(TORCH_DT[cfg.dtype])
         self.lens_dev = torch.from_numpy(self.lens.astype(np.int32)).to(dev)
         self.tables_dev = torch.from_numpy(tables.astype(np.int32)).to(dev)
-        self.attn_dev = torch.from_numpy(attn.astype(np.int32)).to(dev)
-        self.pf_src_dev = [torch.from_numpy(s).to(dev) for s in self.pf_src]
-        self.pf_dst_dev = [torch.from_numpy(d).to(dev) for d in self.pf_dst]
+        self.attn_dev = None
+        self.restage()
         self.local_view = ema.pool_view(self.h, ema.POOL_LOCAL)
         self.slice_view = ema.pool_view(self.h, ema.POOL_SLICE)
         self.host_local = self.host_slice = None
@@ -137,6 +126,33 @@ class Workload:
                 e = min(flat.numel(), s + chunk)
                 flat[s:e].copy_(torch.randn(e - s, generator=g, device="cuda", dtype=torch.float32))
 
+    def restage(self):
+        """Per-layer prefetch lists and attention tables from the canonical
+        tables ``self.tables``: layer l's slice-resident blocks are prefetched, in
+        table order, into staging slot l % staging_slots, and its attention table
+        is the canonical one with each slice id replaced by its staging block."""
+        tables = self.tables
+        self.pf_src, self.pf_dst = [], []
+        attn = tables.copy()
+        for l in range(self.L):
+            mask = tables[l] >= self.n_local
+            src = tables[l][mask]
+            if len(src) > self.stage_n:
+                raise ValueError(f"layer {l}: {len(src)} slice blocks, staging holds {self.stage_n}")
+            dst = self.staging[l % self.staging_slots, :len(src)]
+            attn[l][mask] = dst
+            self.pf_src.append(src.astype(np.int32))
+            self.pf_dst.append(dst.astype(np.int32))
+        self.attn_tables = attn
+        dev = torch.device("cuda")
+        a32 = torch.from_numpy(attn.astype(np.int32))
+        if self.attn_dev is None or self.attn_dev.shape != a32.shape:
+            self.attn_dev = a32.to(dev)
+        else:
+            self.attn_dev.copy_(a32)
+        self.pf_src_dev = [torch.from_numpy(s).to(dev) for s in self.pf_src]
+        self.pf_dst_dev = [torch.from_numpy(d).to(dev) for d in self.pf_dst]
+
     # ---- the hot path ---------------------------------------------------------------
     def prefetch(self, l, stream=None):
         ema.slice_prefetch(self.h, self.pf_src_dev[l], self.pf_dst_dev[l], len(self.pf_src[l]),
@@ -168,6 +184,56 @@ class Workload:
         st.local[:] = self.host_local
         st.slice[:] = self.host_slice
         return st
+
+
+class StepRunner:
+    """One decode step of a workload: for every layer, prefetch of layer l+1 on
+    the copy stream while attention of layer l runs on the attention stream
+    (``mode="serial"``: one stream, copy then attention). Staging slot l % 2 is
+    refilled only after the attention that last read it; attention of layer l
+    waits for its own prefetch. ``timers`` (optional) receives per-layer event
+    pairs: {"pf": [(start, end)] * L, "at": [(start, end)] * L}."""
+
+    def __init__(self, w, mode="overlap"):
+        self.w = w
+        self.s1 = torch.cuda.Stream()
+        self.s2 = torch.cuda.Stream() if mode == "overlap" else self.s1
+        self.ev_pf = [torch.cuda.Event() for _ in range(w.L)]
+        self.ev_at = [torch.cuda.Event() for _ in range(w.L)]
+
+    def new_timers(self):
+        mk = lambda: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        return {"pf": [mk() for _ in range(self.w.L)], "at": [mk() for _ in range(self.w.L)]}
+
+    def _prefetch(self, l, timers):
+        if timers:
+            timers["pf"][l][0].record(self.s2)
+        self.w.prefetch(l, stream=self.s2)
+        if timers:
+            timers["pf"][l][1].record(self.s2)
+        self.ev_pf[l].record(self.s2)
+
+    def run(self, out, timers=None):
+        w, s1, s2 = self.w, self.s1, self.s2
+        L = w.L
+        for l in range(L):
+            if l == 0:
+                # staging slots 0/1 were last read by the previous step's last layers
+                s2.wait_event(self.ev_at[L - 1])
+                if L >= 2:
+                    s2.wait_event(self.ev_at[L - 2])
+                self._prefetch(0, timers)
+            if l + 1 < L:
+                if l >= 1:
+                    s2.wait_event(self.ev_at[l - 1])   # slot (l+1) % 2 was read by layer l-1
+                self._prefetch(l + 1, timers)
+            s1.wait_event(self.ev_pf[l])
+            if timers:
+                timers["at"][l][0].record(s1)
+            w.attention(l, out, stream=s1)
+            if timers:
+                timers["at"][l][1].record(s1)
+            self.ev_at[l].record(s1)
 
 
 def rel_err(out, ref):
