@@ -54,7 +54,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama3-8b-kv",
-                    choices=["llama3-8b-kv", "llama-70b-tp8-share", "bursty-8b"])
+                    choices=["llama3-8b-kv", "llama-70b-tp8-share", "bursty-8b", "stress"])
     ap.add_argument("--mode", default="overlap", choices=["overlap", "serial"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
@@ -207,42 +207,24 @@ def symmetry(w, out, s, reps, ema, torch):
 
 def reclaim_phase(w, s, reps, ema, torch):
     """The lender takes 5 % of its lent blocks back, ``reps`` times. Each call is
-    queued behind a device copy long enough to outlast the call's host planning
-    (sized from an untimed call of the same size, whose slots are lent back), so
-    that the events bracket only device work: upload of the plan, block copies,
-    table rewrite. ``host_plan_ms`` is the call's host time; ``device_only`` says
-    whether the copy was indeed still running when the call returned."""
-    lim = ema.slice_get_info(w.h)["lim"]
-    n0 = max(1, lim // 20)
-    c0 = time.perf_counter()
-    ema.slice_reclaim(w.h, n0, w.tables_dev.view(-1), stream=s)
-    host_s = time.perf_counter() - c0
-    ema.slice_lend(w.h, n0)
-    torch.cuda.synchronize()
-    # about 5 TB/s of copy traffic: 3x the host time, at least 2 GiB, at most 32 GiB
-    nbytes = int(min(32 << 30, max(2 << 30, 3 * host_s * 5e12 / 2)))
-    blk_a = torch.empty(nbytes // 2, dtype=torch.int16, device="cuda")
-    blk_b = torch.empty_like(blk_a)
+    queued behind a device copy long enough to outlast the call's host planning,
+    so the events bracket only device work: upload of the plan, block copies,
+    table rewrite. ``host_plan_ms`` is the call's host time; ``device_only``
+    says whether the copy was indeed still running when the call returned."""
+    from harness import BlockedTimer
+    timer = BlockedTimer()
     res = []
     for _ in range(reps):
         lim = ema.slice_get_info(w.h)["lim"]
         n = max(1, lim // 20)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        with torch.cuda.stream(s):
-            blk_b.copy_(blk_a)
-        e0.record(s)
-        c0 = time.perf_counter()
-        r = ema.slice_reclaim(w.h, n, w.tables_dev.view(-1), stream=s)
-        c1 = time.perf_counter()
-        covered = not e0.query()      # the blocker was still running when the call returned
-        e1.record(s)
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1)
+        r, ms, hms, covered = timer.time(
+            s, lambda: ema.slice_reclaim(w.h, n, w.tables_dev.view(-1), stream=s),
+            host_ms=2.0 + 50e-6 * n)
         nb = 2 * r["moved"] * w.bb + 8 * w.tables_dev.numel()
         res.append({"n": n, "moved": r["moved"], "written_back": r["written_back"],
-                    "victims": len(r["victims"]), "ms": ms, "host_plan_ms": (c1 - c0) * 1e3,
+                    "victims": len(r["victims"]), "ms": ms, "host_plan_ms": hms,
                     "device_only": covered, "GBps": nb / (ms / 1e3) / 1e9})
-    del blk_a, blk_b
+    timer.close()
     return res
 
 
@@ -304,6 +286,50 @@ def bursty_main(args):
     print(json.dumps(res))
 
 
+def stress_main(args):
+    """Large-block copy stress: per block size, prefetch of every slice block in
+    one call, then reclaims of 1, 5, 25 and 100 % of the lent slots (write-back
+    to local), each followed by a migration back; prints one JSON line."""
+    import torch
+    import synth
+    from stress import StressRun, stress_blocks
+
+    torch.cuda.set_device(0)
+    cfg = synth.STRESS
+    out = {}
+    for bs in cfg.extra["block_sizes"]:
+        log(f"stress block size {bs}: {stress_blocks(cfg, bs)} blocks")
+        run = StressRun(bs)
+        try:
+            pf = run.prefetch_all()
+            run.free_staging()
+            rc = run.reclaim_sweep()
+        finally:
+            run.close()
+        torch.cuda.empty_cache()
+        out[str(bs)] = {"blocks": run.N, "block_bytes": run.w.bb, "prefetch": pf,
+                        "reclaim": rc}
+        log(f"bs {bs}: prefetch {pf['GBps']:.0f} GB/s, reclaim "
+            + ", ".join(f"{r['frac']:.0%} {r['GBps']:.0f}" for r in rc))
+    bad = [k for k, v in out.items() if not v["prefetch"]["exact"]
+           or not all(r["exact"] and r["tables_ok"] for r in v["reclaim"])]
+    if bad:
+        raise RuntimeError(f"sampled copies differ at block sizes {bad}")
+    best = max(v["prefetch"]["GBps"] for v in out.values())
+    res = {"metric": "prefetch/reclaim GB/s + paged decode tokens/s, % of HBM roofline, 1 GPU",
+           "value": best, "unit": "GB/s", "n_gpus": 1, "steps": 1, "warmup": 0,
+           "ms_per_step": None, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "f16", "data": "synthetic",
+           "config": {"workload": "stress", "kv_heads": cfg.kv_heads,
+                      "head_dim": cfg.head_dim, "slice_frac": cfg.slice_frac,
+                      "block_sizes": list(cfg.extra["block_sizes"])},
+           "roofline": {"bound": "hbm", "achieved": best, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                        "frac": best / HBM_PEAK_GBPS, "traffic": None,
+                        "kernel": "block_copy_kernel (prefetch of every slice block)"},
+           "sweep": out}
+    print(json.dumps(res))
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -315,6 +341,9 @@ def main():
 
     if args.workload == "bursty-8b":
         bursty_main(args)
+        return
+    if args.workload == "stress":
+        stress_main(args)
         return
     import torch
     import synth

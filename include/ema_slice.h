@@ -110,7 +110,9 @@ typedef struct {
  * is reserved jointly and its segments are assigned one user at a time).
  * Allocates two separate device regions on the current HIP device:
  * floor(local_bytes/block_bytes) local blocks and floor(lent_bytes/block_bytes)
- * slice slots, all FREE, lim = n_slice (everything lent).
+ * slice slots, all FREE, lim = n_slice (everything lent), plus reclaim's plan
+ * buffers (8 bytes per block, pinned host and device), so that reclaim itself
+ * never allocates.
  * flags: EMA_CREATE_HOST_ONLY (no device memory; copy and attention entry
  * points then take host id arrays, validate them and launch nothing) and/or
  * EMA_CREATE_CHECKED.
@@ -198,6 +200,9 @@ int ema_slice_migrate(ema_slice_t h, const int32_t* src_ids, const int32_t* dst_
  * preempted owners in order; moves_src/moves_dst (host [moves_cap], may be
  * NULL): the copies made. Counts beyond a cap are still reported in result.
  * In host-only mode canon_tables must be NULL with n_entries 0.
+ * The plan (8 bytes per moved or released block) is uploaded from the
+ * handle's pinned buffer; a reclaim first waits for the previous reclaim's
+ * upload to finish, never for anything else on the device.
  * Errors: INVAL (n_blocks < 0, n_entries < 0, bad table pointer), HIP.
  */
 int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, int64_t n_entries,

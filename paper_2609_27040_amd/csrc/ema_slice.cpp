@@ -168,6 +168,13 @@ int ema_slice_create(const ema_kv_shape* shape, size_t local_bytes, size_t lent_
   if (e == hipSuccess) e = hipMemset(h->d_err, 0, 4);
   if (e == hipSuccess) e = ema::launch_iota(h->d_remap, n_total, nullptr);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&h->h_work_ev, hipEventDisableTiming);
+  // Reclaim's plan upload: keys and values of at most every block once
+  // (movers and released blocks are disjoint), so reclaim never allocates.
+  const size_t work = size_t(2) * size_t(n_total > 0 ? n_total : 1);
+  if (e == hipSuccess) e = hipHostMalloc(&h->h_work, work * 4, hipHostMallocDefault);
+  if (e == hipSuccess) h->h_work_cap = work;
+  if (e == hipSuccess) e = hipMalloc(&h->d_work, work * 4);
+  if (e == hipSuccess) h->work_cap = work;
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
     const int rc = hip_fail(e, "create");

@@ -177,7 +177,8 @@ def slice_migrate(h, src_ids, dst_ids, n=None, stream=None):
 
 def slice_reclaim(h, n_blocks, canon_tables=None, stream=None, caps=None):
     """canon_tables: int32 device tensor rewritten in place (None for none).
-    Returns the result counts plus the victims and the copies made."""
+    Returns the result counts, the victims (list) and the copies made
+    ("moves": int64 array [moved][2] of (source, destination) unified ids)."""
     info = slice_get_info(h)
     cap = int(caps) if caps is not None else info["n_local"] + info["n_slice"]
     res = ReclaimResult()
@@ -193,7 +194,7 @@ def slice_reclaim(h, n_blocks, canon_tables=None, stream=None, caps=None):
     m = min(res.moved, cap)
     return {"reclaimed": res.reclaimed, "moved": res.moved, "written_back": res.written_back,
             "victims": victims[:min(res.n_victims, cap)].tolist(), "lim": res.lim,
-            "moves": list(zip(msrc[:m].tolist(), mdst[:m].tolist()))}
+            "moves": np.stack([msrc[:m], mdst[:m]], axis=1).astype(np.int64)}
 
 
 def paged_decode_attention(h, q, block_table, seq_lens, out, scale=0.0, stream=None):

@@ -74,6 +74,8 @@ class Workload:
             self._fill_host(rng)
         elif fill == "device":
             self._fill_device(cfg.seed if seed is None else seed)
+        elif fill == "pattern":
+            self._fill_pattern()
         torch.cuda.synchronize()
 
     # ---- values -----------------------------------------------------------------
@@ -152,6 +154,19 @@ class Workload:
             self.attn_dev.copy_(a32)
         self.pf_src_dev = [torch.from_numpy(s).to(dev) for s in self.pf_src]
         self.pf_dst_dev = [torch.from_numpy(d).to(dev) for d in self.pf_dst]
+
+    def _fill_pattern(self):
+        """Every 8-byte word of both pools gets a distinct value (its position,
+        the slice pool offset past the local one): cheap at any size, and any
+        misplaced copy shows. Not attention data (random bit patterns)."""
+        base = 0
+        for view in (self.local_view, self.slice_view):
+            flat = view.view(-1).view(torch.int64)
+            chunk = 1 << 28
+            for s in range(0, flat.numel(), chunk):
+                e = min(flat.numel(), s + chunk)
+                torch.arange(base + s, base + e, dtype=torch.int64, device="cuda", out=flat[s:e])
+            base += flat.numel()
 
     # ---- the hot path ---------------------------------------------------------------
     def prefetch(self, l, stream=None):
@@ -234,6 +249,46 @@ class StepRunner:
             if timers:
                 timers["at"][l][1].record(s1)
             self.ev_at[l].record(s1)
+
+
+class BlockedTimer:
+    """Device time of one library call that also does host work (planning,
+    uploads): the call is queued behind a device copy long enough to outlast
+    its host part, so the events around it bracket device work only. The copy
+    is sized from a host-time estimate (about 5 bytes per ns of copy traffic,
+    three times the estimate, 2 to 32 GiB)."""
+
+    def __init__(self):
+        self.a = self.b = None
+
+    def _blocker(self, host_ms):
+        nbytes = int(min(32 << 30, max(2 << 30, 3 * host_ms * 1e-3 * 5e12 / 2)))
+        if self.a is None or self.a.numel() * 2 < nbytes:
+            self.a = self.b = None
+            self.a = torch.empty(nbytes // 2, dtype=torch.int16, device="cuda")
+            self.b = torch.empty_like(self.a)
+        return self.a[:nbytes // 2], self.b[:nbytes // 2]
+
+    def time(self, stream, call, host_ms=0.0):
+        """Returns (result, device ms, host ms, covered); covered is False when
+        the blocking copy had already finished as the call returned."""
+        import time as _time
+        a, b = self._blocker(host_ms)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(stream):
+            b.copy_(a)
+        e0.record(stream)
+        c0 = _time.perf_counter()
+        r = call()
+        c1 = _time.perf_counter()
+        covered = not e0.query()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return r, e0.elapsed_time(e1), (c1 - c0) * 1e3, covered
+
+    def close(self):
+        self.a = self.b = None
 
 
 def rel_err(out, ref):

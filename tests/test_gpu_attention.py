@@ -65,7 +65,8 @@ def test_tiny_config_end_to_end(ema, layout):
         # reclaim everything lent; tables rewritten on the device
         r = ema.slice_reclaim(w.h, 10 ** 9, w.tables_dev.view(-1))
         ro = st.reclaim(10 ** 9, w.tables)
-        assert r["moves"] == ro["moves"] and r["victims"] == ro["victims"]
+        assert np.array_equal(r["moves"], np.asarray(ro["moves"], np.int64).reshape(-1, 2))
+        assert r["victims"] == ro["victims"]
         assert r["lim"] == 0 and ro["lim"] == 0
         assert np.array_equal(w.tables_dev.cpu().numpy(), w.tables)
         torch.cuda.synchronize()

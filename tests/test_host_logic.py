@@ -55,7 +55,7 @@ class LibHostBackend:
         own_l, own_s, _ = self.ema.slice_owners(self.h)
         owners_before = np.concatenate([own_l, own_s])
         r = self.ema.slice_reclaim(self.h, n)
-        remap = {s: d for s, d in r["moves"]}
+        remap = {int(s): int(d) for s, d in r["moves"]}
         victims = set(r["victims"])
         flat = tables.reshape(-1)
         for i, t in enumerate(flat):

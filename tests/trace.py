@@ -163,8 +163,9 @@ def _assert_same(a, b, what):
         for k in a:
             _assert_same(a[k], b[k], f"{what}.{k}")
     elif isinstance(a, (list, tuple, np.ndarray)):
-        assert np.array_equal(np.asarray(a, dtype=np.int64), np.asarray(b, dtype=np.int64)), \
-            f"{what}: {a} != {b}"
+        # pair lists compare flattened, so [] equals an empty [0][2] array
+        assert np.array_equal(np.asarray(a, dtype=np.int64).reshape(-1),
+                              np.asarray(b, dtype=np.int64).reshape(-1)), f"{what}: {a} != {b}"
     else:
         assert a == b, f"{what}: {a} != {b}"
 
