@@ -8,7 +8,11 @@
 // change layout go through the wave's LDS tile: K rows only change order
 // (256-byte rows are re-addressed, no LDS), V is transposed between
 // [token][channel] (NHD) and [channel][token] (ATTN) in LDS so that both the
-// global reads and the global writes stay 16 bytes per lane.
+// global reads and the global writes stay 16 bytes per lane. Into ATTN, a V
+// unit is all BS tokens of 2048/BS channels, so every transposed row it writes
+// is whole; out of ATTN it is 16 tokens of all 128 channels, so every token
+// row it writes is whole. The tile is dynamic LDS, requested only when the
+// slice layout differs from the local one.
 #include "kernels.h"
 
 namespace ema {
@@ -19,6 +23,12 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kUnitBytes = 4096;
 constexpr int kWaves = 4;
 constexpr int kTileRow = 128 + 8;   // u16 per LDS tile row (padded, keeps 16 B alignment)
+
+// u16 per wave of the relayout tile: 16 x kTileRow (out of ATTN) or
+// BS x (2048/BS + 8) (into ATTN).
+__host__ __device__ constexpr int tile_elems(int bs) {
+  return 16 * kTileRow > 2048 + 8 * bs ? 16 * kTileRow : 2048 + 8 * bs;
+}
 
 // Block data is touched once per copy: streaming (non-temporal) loads and
 // stores keep it from displacing other data in L2 and the memory-side cache,
@@ -39,7 +49,7 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
                                                          const int32_t* __restrict__ src_ids,
                                                          const int32_t* __restrict__ dst_ids,
                                                          int32_t n, int32_t* err_count) {
-  __shared__ __attribute__((aligned(16))) uint16_t tile[kWaves][16][kTileRow];
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds_tile[];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int upb = int(pv.block_bytes / kUnitBytes);
@@ -76,7 +86,8 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
     return;
   }
 
-  // Layout change. Unit k -> (half, head h, 16-token group tg).
+  // Layout change. Unit k -> (half, head h, group tg): a 16-token group, or
+  // for V into ATTN a group of 2048/BS channels (BS/16 groups either way).
   const int H = pv.kv_heads;
   const int BS = pv.block_size;
   const int tgs = BS / 16;
@@ -105,38 +116,43 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
     return;
   }
 
-  uint16_t (*T)[kTileRow] = tile[wave];
+  uint16_t* tw = lds_tile + wave * tile_elems(BS);
   const char* sv = sb + half_bytes;
   char* dv = db + half_bytes;
   if (s_nhd) {
-    // NHD -> ATTN. Read 16 token rows (8 channels per lane) into T[t][c].
-    u32x4 v[4];
+    // NHD -> ATTN, unit (h, channel group tg): all BS tokens of C = 2048/BS
+    // channels. Read C channels of every token row (LR lanes per row) into the
+    // tile as [t][c], then write C whole transposed rows of BS tokens (LC lanes
+    // each).
+    const int C = 2048 / BS;
+    const int c0 = tg * C;
+    const int LR = C / 8;
+    const int stride = C + 8;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int tl = j * 4 + (lane >> 4);
-      v[j] = ld16(sv + int64_t((tg * 16 + tl) * H + h) * 256 + (lane & 15) * 16);
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int tl = j * 4 + (lane >> 4);
-      *reinterpret_cast<u32x4*>(&T[tl][(lane & 15) * 8]) = v[j];
+      const int t = j * (64 / LR) + lane / LR;
+      const int c = (lane % LR) * 8;
+      const u32x4 v = ld16(sv + (int64_t(t * H + h) * 128 + c0 + c) * 2);
+      *reinterpret_cast<u32x4*>(&tw[t * stride + c]) = v;
     }
     wave_lds_sync();
-    // Write 128 channel rows x 16 tokens: item = (c, 8-token half).
+    const int LC = BS / 8;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int item = j * 64 + lane;
-      const int c = item >> 1;
-      const int t0 = (item & 1) * 8;
+      const int cc = item / LC;
+      const int t0 = (item % LC) * 8;
       uint32_t w[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        w[q] = uint32_t(T[t0 + 2 * q][c]) | (uint32_t(T[t0 + 2 * q + 1][c]) << 16);
-      u32x4 out = {w[0], w[1], w[2], w[3]};
-      st16(dv + (int64_t(h * 128 + c) * BS + tg * 16 + t0) * 2, out);
+        w[q] = uint32_t(tw[(t0 + 2 * q) * stride + cc]) |
+               (uint32_t(tw[(t0 + 2 * q + 1) * stride + cc]) << 16);
+      const u32x4 out = {w[0], w[1], w[2], w[3]};
+      st16(dv + (int64_t(h * 128 + c0 + cc) * BS + t0) * 2, out);
     }
   } else {
-    // ATTN -> NHD. Read 128 channel rows x 16 tokens, scatter into T[t][c].
+    // ATTN -> NHD. Read 128 channel rows x 16 tokens, scatter into the tile as
+    // [t][c], then write 16 whole token rows.
     u32x4 v[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -153,15 +169,15 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
       const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        T[t0 + 2 * q][c] = uint16_t(w[q] & 0xffffu);
-        T[t0 + 2 * q + 1][c] = uint16_t(w[q] >> 16);
+        tw[(t0 + 2 * q) * kTileRow + c] = uint16_t(w[q] & 0xffffu);
+        tw[(t0 + 2 * q + 1) * kTileRow + c] = uint16_t(w[q] >> 16);
       }
     }
     wave_lds_sync();
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int tl = j * 4 + (lane >> 4);
-      const u32x4 out = *reinterpret_cast<const u32x4*>(&T[tl][(lane & 15) * 8]);
+      const u32x4 out = *reinterpret_cast<const u32x4*>(&tw[tl * kTileRow + (lane & 15) * 8]);
       st16(dv + int64_t((tg * 16 + tl) * H + h) * 256 + (lane & 15) * 16, out);
     }
   }
@@ -200,7 +216,8 @@ hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32
   if (n <= 0) return hipSuccess;
   const int64_t units = int64_t(n) * (pv.block_bytes / kUnitBytes);
   const int64_t grid = (units + kWaves - 1) / kWaves;
-  hipLaunchKernelGGL(block_copy_kernel, dim3(unsigned(grid)), dim3(256), 0, stream, pv, src, dst,
+  const size_t lds = pv.slice_layout == 0 ? 0 : size_t(kWaves) * tile_elems(pv.block_size) * 2;
+  hipLaunchKernelGGL(block_copy_kernel, dim3(unsigned(grid)), dim3(256), lds, stream, pv, src, dst,
                      n, err_count);
   return hipGetLastError();
 }

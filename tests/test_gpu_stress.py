@@ -23,7 +23,7 @@ def ema():
 
 
 @pytest.mark.parametrize("bs,layout,n_blocks", [(16, 0, None), (64, 0, None), (256, 0, None),
-                                                (16, 1, 65536), (64, 1, 16384)])
+                                                (16, 1, 65536), (64, 1, 16384), (256, 1, 4096)])
 def test_stress_prefetch_and_reclaim_sweep(ema, bs, layout, n_blocks):
     from stress import StressRun
     print(f"stress bs={bs} layout={layout} n_blocks={n_blocks}", flush=True)
@@ -33,12 +33,15 @@ def test_stress_prefetch_and_reclaim_sweep(ema, bs, layout, n_blocks):
         assert pf["exact"], "prefetch: sampled blocks differ"
         run.free_staging()
         lim0 = ema.slice_get_info(run.w.h)["lim"]
-        for r in run.reclaim_sweep():
+        sweep = run.reclaim_sweep()
+        for r in sweep:
             assert r["tables_ok"], f"{r['frac']}: device tables differ"
             assert r["exact"], f"{r['frac']}: sampled written-back blocks differ"
             assert r["moved"] == r["n"] == r["written_back"] and r["victims"] == 0, r
             assert ema.slice_get_info(run.w.h)["lim"] == lim0     # lent back after each
-        print(f"prefetch {pf['GBps']:.0f} GB/s", flush=True)
+        print(f"prefetch {pf['GBps']:.0f} GB/s; reclaim "
+              + ", ".join(f"{r['frac']:.0%} {r['GBps']:.0f} (back {r['migrate_back_GBps']:.0f})"
+                          for r in sweep), flush=True)
         assert ema.slice_device_errors(run.w.h) == 0
     finally:
         run.close()
