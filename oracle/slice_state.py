@@ -25,6 +25,12 @@ Operations (each all-or-nothing; on error nothing changes):
   the slice process prefetches ahead of access).
 * migrate: move a logical block between pools (copy to a block of the same
   owner).
+* kv_append / writeback: a decode step stores each sequence's new token in the
+  block holding its position (a slice-resident block is written through its
+  staged copy), and the modified staged copies are copied back into their
+  slice blocks -- the swap-out that matches the swap-in (section 4: data
+  swapped in must be balanced by data swapped out; here only blocks written
+  since their prefetch need to travel).
 * reclaim(n): the lender takes back n lent slots (section 4.1). It operates on
   logical ownership: borrowed blocks in the returned range move to free space
   when there is room; otherwise whole requests are preempted, and a preempted
@@ -34,7 +40,7 @@ Operations (each all-or-nothing; on error nothing changes):
 from collections import Counter
 import numpy as np
 
-from .layout import LAYOUT_ATTN, block_bytes, convert_block
+from .layout import LAYOUT_ATTN, block_bytes, convert_block, decode_block, encode_block
 
 FREE, STAGING, LENDER = -1, -2, -3
 LOCAL, SLICE = 0, 1
@@ -194,6 +200,47 @@ class SliceOracle:
                 raise OracleError(ERR_INVAL, f"migrate {s}->{d}: owners differ or unowned")
         for s, d in zip(src, dst):
             self._copy(s, d)
+
+    def writeback(self, src, dst):
+        """Swap-out of modified staged copies: copy STAGING local blocks src[i]
+        back into owned slice blocks dst[i], re-laid into the slice layout (the
+        inverse of prefetch; only blocks written since their prefetch need it)."""
+        src, dst = self._check_pairs(src, dst)
+        for u in src:
+            if u >= self.n_local or self.owner(u) != STAGING:
+                raise OracleError(ERR_INVAL, f"writeback source {u} is not a staging block")
+        for u in dst:
+            if u < self.n_local or self.owner(u) < 0:
+                raise OracleError(ERR_INVAL, f"writeback destination {u} is not an owned slice block")
+        for s, d in zip(src, dst):
+            self._copy(s, d)
+
+    def kv_append(self, k16, v16, table, lens):
+        """Store the new decode token of every sequence: for sequence b with
+        lens[b] > 0 the token at position p = lens[b] - 1 (lens already count
+        it) gets K = k16[b], V = v16[b] (uint16 [kv_head][channel]) in row
+        p % block_size of local block table[b][p // block_size]. Every target
+        must be a local block; nothing is written otherwise."""
+        table = np.asarray(table)
+        targets = []
+        for b, n in enumerate(np.asarray(lens)):
+            n = int(n)
+            if n <= 0:
+                continue
+            p = n - 1
+            j = p // self.block_size
+            if j >= table.shape[1]:
+                raise OracleError(ERR_INVAL, f"append: sequence {b} needs block {j}")
+            u = int(table[b, j])
+            if not (0 <= u < self.n_local):
+                raise OracleError(ERR_INVAL, f"append: block {u} of sequence {b} is not local")
+            targets.append((b, u, p % self.block_size))
+        for b, u, r in targets:
+            K, V = decode_block(self.local[u], LAYOUT_ATTN, self.kv_heads, self.head_dim,
+                                self.block_size)
+            K[:, r, :] = k16[b]
+            V[:, r, :] = v16[b]
+            self.local[u] = encode_block(K, V, LAYOUT_ATTN)
 
     # ---- reclaim -------------------------------------------------------------
     def _movers(self, cut):
