@@ -180,6 +180,35 @@ int ema_slice_migrate(ema_slice_t h, const int32_t* src_ids, const int32_t* dst_
                       void* stream);
 
 /*
+ * slice_writeback -- swap-out of modified staged copies (section 4: data swapped
+ * in must be matched by data swapped out; since a prefetch leaves the slice
+ * block in place, only blocks written since their prefetch need to travel).
+ * For i < n: slice block slice_ids[i] <- local block staging_ids[i], re-laid
+ * from EMA_LAYOUT_ATTN into the slice layout. staging_ids: device [n] unified
+ * ids of EMA_STAGING local blocks; slice_ids: device [n] unified ids of owned
+ * slice slots, no duplicates. Async on `stream`.
+ * Errors (checked mode or host-only): INVAL for any violation above.
+ */
+int ema_slice_writeback(ema_slice_t h, const int32_t* staging_ids, const int32_t* slice_ids,
+                        int32_t n, void* stream);
+
+/*
+ * kv_append -- a decode step stores each sequence's new token before attention
+ * reads it: for sequence b with seq_lens[b] > 0 (lengths already counting the
+ * new token), the token at position p = seq_lens[b] - 1 gets K = k_new[b] and
+ * V = v_new[b] in row p % block_size of local block block_table[b][p /
+ * block_size]. block_table is an attention table (device [batch][max_blocks]
+ * local ids): a slice-resident block is named by its staged copy, which the
+ * caller then writes back with ema_slice_writeback. k_new, v_new: device
+ * [batch][num_kv_heads][head_dim] in the slice's dtype. Async on `stream`.
+ * Rows whose block index is >= max_blocks or whose id is not a local block are
+ * skipped and counted (ema_slice_device_errors); checked mode rejects them on
+ * the host first (INVAL), and host-only mode validates host arrays.
+ */
+int ema_kv_append(ema_slice_t h, const void* k_new, const void* v_new, const int32_t* block_table,
+                  const int32_t* seq_lens, int32_t batch, int32_t max_blocks, void* stream);
+
+/*
  * slice_reclaim -- the lender takes back n_blocks lent slots (section 4.1:
  * reclamation works on logical ownership and preempts the borrower's requests
  * until the allocation is satisfied; a preempted request releases its local

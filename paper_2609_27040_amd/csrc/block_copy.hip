@@ -183,6 +183,35 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
   }
 }
 
+// One workgroup per (sequence, KV head), one thread per channel: the K element
+// goes to the token's row, the V element to the token's column of the
+// transposed V rows.
+__global__ __launch_bounds__(128) void kv_append_kernel(PoolView pv, const uint16_t* __restrict__ k_new,
+                                                        const uint16_t* __restrict__ v_new,
+                                                        const int32_t* __restrict__ table,
+                                                        const int32_t* __restrict__ seq_lens,
+                                                        int32_t max_blocks, int32_t* err_count) {
+  const int b = blockIdx.x;
+  const int h = blockIdx.y;
+  const int d = threadIdx.x;
+  const int H = pv.kv_heads;
+  const int BS = pv.block_size;
+  const int len = seq_lens[b];
+  if (len <= 0) return;
+  const int p = len - 1;
+  const int j = p / BS;
+  const int32_t id = j < max_blocks ? table[int64_t(b) * max_blocks + j] : -1;
+  if (id < 0 || id >= pv.n_local) {
+    if (h == 0 && d == 0) atomicAdd(err_count, 1);
+    return;
+  }
+  const int r = p - j * BS;
+  uint16_t* blk = reinterpret_cast<uint16_t*>(pv.local + int64_t(id) * pv.block_bytes);
+  const int64_t src = (int64_t(b) * H + h) * 128 + d;
+  blk[(int64_t(h) * BS + r) * 128 + d] = k_new[src];
+  blk[int64_t(BS) * H * 128 + (int64_t(h) * 128 + d) * BS + r] = v_new[src];
+}
+
 __global__ void remap_scatter_kernel(int32_t* __restrict__ remap, int32_t n_total,
                                      const int32_t* __restrict__ keys,
                                      const int32_t* __restrict__ vals, int32_t n) {
@@ -219,6 +248,16 @@ hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32
   const size_t lds = pv.slice_layout == 0 ? 0 : size_t(kWaves) * tile_elems(pv.block_size) * 2;
   hipLaunchKernelGGL(block_copy_kernel, dim3(unsigned(grid)), dim3(256), lds, stream, pv, src, dst,
                      n, err_count);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_append(const PoolView& pv, const void* k_new, const void* v_new,
+                            const int32_t* table, const int32_t* seq_lens, int32_t batch,
+                            int32_t max_blocks, int32_t* err_count, hipStream_t stream) {
+  if (batch <= 0) return hipSuccess;
+  hipLaunchKernelGGL(kv_append_kernel, dim3(unsigned(batch), unsigned(pv.kv_heads)), dim3(128), 0,
+                     stream, pv, static_cast<const uint16_t*>(k_new),
+                     static_cast<const uint16_t*>(v_new), table, seq_lens, max_blocks, err_count);
   return hipGetLastError();
 }
 

@@ -240,16 +240,28 @@ int ema_slice_lend(ema_slice_t h, int32_t n_blocks, int32_t* added) {
   return rc ? fail(rc, err) : EMA_OK;
 }
 
+enum class CopyKind { kPrefetch, kMigrate, kWriteback };
+
+static int check_copy(const ema_slice* h, CopyKind kind, const int32_t* src, const int32_t* dst,
+                      int32_t n, std::string* err) {
+  switch (kind) {
+    case CopyKind::kPrefetch: return h->book.check_prefetch(src, dst, n, err);
+    case CopyKind::kMigrate: return h->book.check_migrate(src, dst, n, err);
+    default: return h->book.check_writeback(src, dst, n, err);
+  }
+}
+
 static int copy_entry(ema_slice_t h, const int32_t* src, const int32_t* dst, int32_t n,
-                      void* stream, bool prefetch) {
-  const char* what = prefetch ? "prefetch" : "migrate";
+                      void* stream, CopyKind kind) {
+  const char* what = kind == CopyKind::kPrefetch ? "prefetch"
+                     : kind == CopyKind::kMigrate ? "migrate"
+                                                  : "writeback";
   if (!h) return fail(EMA_ERR_INVAL, std::string(what) + ": NULL handle");
   if (n < 0 || (n > 0 && (!src || !dst)))
     return fail(EMA_ERR_INVAL, std::string(what) + ": n < 0 or NULL array");
   std::string err;
   if (h->host_only) {
-    const int rc = prefetch ? h->book.check_prefetch(src, dst, n, &err)
-                            : h->book.check_migrate(src, dst, n, &err);
+    const int rc = check_copy(h, kind, src, dst, n, &err);
     return rc ? fail(rc, err) : EMA_OK;
   }
   if (n == 0) return EMA_OK;
@@ -259,8 +271,7 @@ static int copy_entry(ema_slice_t h, const int32_t* src, const int32_t* dst, int
   if (h->checked) {
     std::vector<int32_t> hs, hd;
     if ((rc = fetch_ints(src, n, st, &hs)) || (rc = fetch_ints(dst, n, st, &hd))) return rc;
-    rc = prefetch ? h->book.check_prefetch(hs.data(), hd.data(), n, &err)
-                  : h->book.check_migrate(hs.data(), hd.data(), n, &err);
+    rc = check_copy(h, kind, hs.data(), hd.data(), n, &err);
     if (rc) return fail(rc, err);
   }
   HIP_TRY(ema::launch_block_copy(pool_view(h), src, dst, n, h->d_err, st), what);
@@ -269,12 +280,54 @@ static int copy_entry(ema_slice_t h, const int32_t* src, const int32_t* dst, int
 
 int ema_slice_prefetch(ema_slice_t h, const int32_t* block_ids, const int32_t* dst_block_table,
                        int32_t n, void* stream) {
-  return copy_entry(h, block_ids, dst_block_table, n, stream, true);
+  return copy_entry(h, block_ids, dst_block_table, n, stream, CopyKind::kPrefetch);
 }
 
 int ema_slice_migrate(ema_slice_t h, const int32_t* src_ids, const int32_t* dst_ids, int32_t n,
                       void* stream) {
-  return copy_entry(h, src_ids, dst_ids, n, stream, false);
+  return copy_entry(h, src_ids, dst_ids, n, stream, CopyKind::kMigrate);
+}
+
+int ema_slice_writeback(ema_slice_t h, const int32_t* staging_ids, const int32_t* slice_ids,
+                        int32_t n, void* stream) {
+  return copy_entry(h, staging_ids, slice_ids, n, stream, CopyKind::kWriteback);
+}
+
+int ema_kv_append(ema_slice_t h, const void* k_new, const void* v_new, const int32_t* block_table,
+                  const int32_t* seq_lens, int32_t batch, int32_t max_blocks, void* stream) {
+  if (!h) return fail(EMA_ERR_INVAL, "append: NULL handle");
+  if (batch < 0 || max_blocks < 0) return fail(EMA_ERR_INVAL, "append: bad batch or max_blocks");
+  if (batch > 0 && (!k_new || !v_new || !block_table || !seq_lens))
+    return fail(EMA_ERR_INVAL, "append: NULL array");
+  if (batch > 65535) return fail(EMA_ERR_INVAL, "append: batch too large");
+  const int32_t bs = h->shape.block_size;
+  auto check = [&](const int32_t* lens, const int32_t* tab) -> int {
+    for (int32_t b = 0; b < batch; ++b) {
+      if (lens[b] <= 0) continue;
+      const int32_t j = (lens[b] - 1) / bs;
+      if (j >= max_blocks) return fail(EMA_ERR_INVAL, "append: position past the block table");
+      const int32_t id = tab[size_t(b) * max_blocks + j];
+      if (id < 0 || id >= h->book.n_local())
+        return fail(EMA_ERR_INVAL, "append: target is not a local block");
+    }
+    return EMA_OK;
+  };
+  if (h->host_only) return batch ? check(seq_lens, block_table) : EMA_OK;
+  if (batch == 0) return EMA_OK;
+  int rc = use_device(h);
+  if (rc) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (h->checked) {
+    std::vector<int32_t> lens, tab;
+    if ((rc = fetch_ints(seq_lens, batch, st, &lens)) ||
+        (rc = fetch_ints(block_table, int64_t(batch) * max_blocks, st, &tab)))
+      return rc;
+    if ((rc = check(lens.data(), tab.data()))) return rc;
+  }
+  HIP_TRY(ema::launch_kv_append(pool_view(h), k_new, v_new, block_table, seq_lens, batch,
+                                max_blocks, h->d_err, st),
+          "append launch");
+  return EMA_OK;
 }
 
 int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, int64_t n_entries,

@@ -24,6 +24,13 @@ struct PoolView {
 hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32_t* dst,
                              int32_t n, int32_t* err_count, hipStream_t stream);
 
+// New decode token of every sequence into its block (ATTN layout): row
+// (len-1) % bs of local block table[b][(len-1) / bs], len = seq_lens[b] > 0.
+// Out-of-range block indices or ids are skipped and counted in *err_count.
+hipError_t launch_kv_append(const PoolView& pv, const void* k_new, const void* v_new,
+                            const int32_t* table, const int32_t* seq_lens, int32_t batch,
+                            int32_t max_blocks, int32_t* err_count, hipStream_t stream);
+
 // remap[keys[i]] = vals[i] for i < n (keys checked against n_total).
 hipError_t launch_remap_scatter(int32_t* remap, int32_t n_total, const int32_t* keys,
                                 const int32_t* vals, int32_t n, hipStream_t stream);

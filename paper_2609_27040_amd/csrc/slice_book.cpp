@@ -216,6 +216,23 @@ int SliceBook::check_migrate(const int32_t* src, const int32_t* dst, int32_t n,
   return kOk;
 }
 
+int SliceBook::check_writeback(const int32_t* src, const int32_t* dst, int32_t n,
+                               std::string* err) const {
+  int rc = check_pairs(src, dst, n, err);
+  if (rc) return rc;
+  for (int32_t i = 0; i < n; ++i)
+    if (src[i] >= n_local_ || owner(src[i]) != kStaging) {
+      *err = "writeback: source " + std::to_string(src[i]) + " is not a staging block";
+      return kErrInval;
+    }
+  for (int32_t i = 0; i < n; ++i)
+    if (dst[i] < n_local_ || owner(dst[i]) < 0) {
+      *err = "writeback: destination " + std::to_string(dst[i]) + " is not an owned slice block";
+      return kErrInval;
+    }
+  return kOk;
+}
+
 int SliceBook::reclaim(int32_t n, ReclaimPlan* p, std::string* err) {
   if (n < 0) {
     *err = "reclaim: n < 0";

@@ -67,6 +67,7 @@ class SliceBook {
   // Copy-list checks (pure reads of state).
   int check_prefetch(const int32_t* src, const int32_t* dst, int32_t n, std::string* err) const;
   int check_migrate(const int32_t* src, const int32_t* dst, int32_t n, std::string* err) const;
+  int check_writeback(const int32_t* src, const int32_t* dst, int32_t n, std::string* err) const;
   // Plans reclaim(n) and commits it to the owner tags.
   int reclaim(int32_t n, ReclaimPlan* plan, std::string* err);
 

@@ -64,6 +64,8 @@ def _load():
         "ema_slice_lend": [P, I32, ctypes.POINTER(I32)],
         "ema_slice_prefetch": [P, P, P, I32, P],
         "ema_slice_migrate": [P, P, P, I32, P],
+        "ema_slice_writeback": [P, P, P, I32, P],
+        "ema_kv_append": [P, P, P, P, P, I32, I32, P],
         "ema_slice_reclaim": [P, I32, P, I64, P, ctypes.POINTER(ReclaimResult), P, I32, P, P, I32],
         "ema_paged_decode_attention": [P, P, P, P, I32, I32, I32, ctypes.c_float, P, P],
         "ema_slice_device_errors": [P, ctypes.POINTER(I32)],
@@ -173,6 +175,30 @@ def slice_migrate(h, src_ids, dst_ids, n=None, stream=None):
         src_ids, dst_ids = _i32_host(src_ids), _i32_host(dst_ids)
     _check(_lib.ema_slice_migrate(h, _ptr(src_ids), _ptr(dst_ids), int(n),
                                   None if host else _stream(stream)))
+
+
+def slice_writeback(h, staging_ids, slice_ids, n=None, stream=None):
+    """staging_ids, slice_ids: int32 device tensors (numpy arrays for a
+    host-only slice)."""
+    n = len(staging_ids) if n is None else n
+    host = isinstance(staging_ids, np.ndarray)
+    if host:
+        staging_ids, slice_ids = _i32_host(staging_ids), _i32_host(slice_ids)
+    _check(_lib.ema_slice_writeback(h, _ptr(staging_ids), _ptr(slice_ids), int(n),
+                                    None if host else _stream(stream)))
+
+
+def kv_append(h, k_new, v_new, block_table, seq_lens, stream=None):
+    """k_new, v_new [B][Hkv][D] (16-bit), block_table int32 [B][max_blocks],
+    seq_lens int32 [B] counting the new token: device tensors (numpy arrays
+    for a host-only slice)."""
+    host = isinstance(block_table, np.ndarray)
+    B = int(block_table.shape[0])
+    max_blocks = int(block_table.shape[1]) if block_table.ndim == 2 else 0
+    if host:
+        block_table, seq_lens = _i32_host(block_table), _i32_host(seq_lens)
+    _check(_lib.ema_kv_append(h, _ptr(k_new), _ptr(v_new), _ptr(block_table), _ptr(seq_lens), B,
+                              max_blocks, None if host else _stream(stream)))
 
 
 def slice_reclaim(h, n_blocks, canon_tables=None, stream=None, caps=None):

@@ -64,6 +64,9 @@ class GpuBackend:
     def prefetch(self, src, dst):
         self.ema.slice_prefetch(self.h, i32(src), i32(dst))
 
+    def writeback(self, src, dst):
+        self.ema.slice_writeback(self.h, i32(src), i32(dst))
+
     def reclaim(self, n, tables):
         t = i32(tables.reshape(-1))
         r = self.ema.slice_reclaim(self.h, n, t)

@@ -26,6 +26,8 @@ class LibHostBackend:
     """The library in host-only mode. Table rewriting is the device's job, so
     this adapter applies the returned plan to host tables itself."""
 
+    validating = True     # host-only slices validate every id list
+
     def __init__(self, n_local, n_slice, layout=0):
         from paper_2609_27040_amd import ema
         self.ema = ema
@@ -50,6 +52,9 @@ class LibHostBackend:
 
     def prefetch(self, src, dst):
         self.ema.slice_prefetch(self.h, np.asarray(src), np.asarray(dst))
+
+    def writeback(self, src, dst):
+        self.ema.slice_writeback(self.h, np.asarray(src), np.asarray(dst))
 
     def reclaim(self, n, tables):
         own_l, own_s, _ = self.ema.slice_owners(self.h)

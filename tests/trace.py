@@ -6,7 +6,7 @@ backend while random operations run: sequences grow and finish, blocks migrate
 between pools, prefetches run, the lender lends and reclaims.
 
 Backends expose: alloc_blocks(where, owners) -> ids, free_blocks(ids),
-lend(n) -> added, migrate(src, dst), prefetch(src, dst),
+lend(n) -> added, migrate(src, dst), prefetch(src, dst), writeback(src, dst),
 reclaim(n, tables) -> dict, owners() -> (own_local, own_slice, lim).
 Errors are raised as exceptions carrying ``.code``.
 """
@@ -17,6 +17,8 @@ STAGING = -2
 
 
 class OracleBackend:
+    validating = True     # rejects invalid id lists (device backends may not)
+
     def __init__(self, st):
         self.st = st
 
@@ -34,6 +36,9 @@ class OracleBackend:
 
     def prefetch(self, src, dst):
         self.st.prefetch(src, dst)
+
+    def writeback(self, src, dst):
+        self.st.writeback(src, dst)
 
     def reclaim(self, n, tables):
         r = self.st.reclaim(n, tables)
@@ -133,6 +138,13 @@ class Cache:
         assert err is None, err
         if check is not None:
             check(src, [int(u) for u in dst])
+        # the staged copies go back (a decode step that wrote them); where every
+        # backend validates ids, a wrong direction is refused by all alike
+        _, err = self._all("writeback", [int(u) for u in dst], src)
+        assert err is None, err
+        if all(getattr(be, "validating", False) for be in self.backends):
+            _, err = self._all("writeback", src, [int(u) for u in dst])
+            assert err is not None, "writeback from a slice block into staging was accepted"
         _, err = self._all("free_blocks", dst)
         assert err is None, err
 
