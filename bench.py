@@ -7,7 +7,9 @@ block 16, batch 64, lengths U[1024, 4096], 30 % of each layer's blocks in the
 slice). Per layer: the slice-resident blocks of layer l+1 are prefetched into a
 double-buffered staging area on one stream while paged decode attention of
 layer l runs on another (``--mode serial`` runs both on one stream: copy, then
-attention, the on-demand swap of the paper's ablation).
+attention, the on-demand swap of the paper's ablation; ``--append`` also stores
+a new token per sequence before each layer's attention and writes the modified
+staged blocks back to the slice after it).
 
 After the timed steps, untimed by the step clock:
   * symmetry: attention over every layer through the staged tables versus
@@ -56,6 +58,9 @@ def parse():
     ap.add_argument("--workload", default="llama3-8b-kv",
                     choices=["llama3-8b-kv", "llama-70b-tp8-share", "bursty-8b", "stress"])
     ap.add_argument("--mode", default="overlap", choices=["overlap", "serial"])
+    ap.add_argument("--append", action="store_true",
+                    help="each layer also appends the new token's K/V and writes the modified "
+                         "staged blocks back to the slice")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--reclaim-reps", type=int, default=4)
@@ -360,7 +365,7 @@ def main():
     w = Workload(cfg, fill="device", extra_local=extra)
     L, B = w.L, w.B
     log(f"{L} layers, batch {B}, {w.n_local} local + {w.slice_view.shape[0]} slice blocks")
-    runner = StepRunner(w, args.mode)
+    runner = StepRunner(w, args.mode, append=args.append)
     s1 = runner.s1
     out = w.new_out()
     attn_b = attention_bytes(w)
@@ -413,7 +418,7 @@ def main():
         "config": {"workload": cfg.name, "layers": L, "batch": B, "q_heads": cfg.q_heads,
                    "kv_heads": cfg.kv_heads, "head_dim": cfg.head_dim,
                    "block_size": cfg.block_size, "lens": list(cfg.lens),
-                   "slice_frac": cfg.slice_frac, "mode": args.mode},
+                   "slice_frac": cfg.slice_frac, "mode": args.mode, "append": args.append},
         "roofline": {"bound": "hbm", "achieved": attn_gbps, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": attn_gbps / HBM_PEAK_GBPS, "traffic": traffic,
                      "kernel": "paged_decode_attention (attn_mfma_streamk + attn_combine_streamk)"},

@@ -146,6 +146,16 @@ class Workload:
             self.pf_src.append(src.astype(np.int32))
             self.pf_dst.append(dst.astype(np.int32))
         self.attn_tables = attn
+        # blocks a decode-step append writes: each sequence's last block; those
+        # in the slice are written through their staged copy and written back
+        self.wb_src, self.wb_dst = [], []
+        rows = np.arange(self.B)
+        last = np.maximum(self.lens - 1, 0) // self.bs
+        for l in range(self.L):
+            canon = tables[l, rows, last] if self.B else np.zeros(0, np.int64)
+            dirty = (canon >= self.n_local) & (self.lens > 0)
+            self.wb_src.append(attn[l, rows, last][dirty].astype(np.int32))
+            self.wb_dst.append(canon[dirty].astype(np.int32))
         dev = torch.device("cuda")
         a32 = torch.from_numpy(attn.astype(np.int32))
         if self.attn_dev is None or self.attn_dev.shape != a32.shape:
@@ -154,6 +164,8 @@ class Workload:
             self.attn_dev.copy_(a32)
         self.pf_src_dev = [torch.from_numpy(s).to(dev) for s in self.pf_src]
         self.pf_dst_dev = [torch.from_numpy(d).to(dev) for d in self.pf_dst]
+        self.wb_src_dev = [torch.from_numpy(s).to(dev) for s in self.wb_src]
+        self.wb_dst_dev = [torch.from_numpy(d).to(dev) for d in self.wb_dst]
 
     def _fill_pattern(self):
         """Every 8-byte word of both pools gets a distinct value (its position,
@@ -172,6 +184,22 @@ class Workload:
     def prefetch(self, l, stream=None):
         ema.slice_prefetch(self.h, self.pf_src_dev[l], self.pf_dst_dev[l], len(self.pf_src[l]),
                            stream=stream)
+
+    def append(self, l, k_new, v_new, stream=None):
+        ema.kv_append(self.h, k_new, v_new, self.attn_dev[l], self.lens_dev, stream=stream)
+
+    def writeback(self, l, stream=None):
+        ema.slice_writeback(self.h, self.wb_src_dev[l], self.wb_dst_dev[l], len(self.wb_src[l]),
+                            stream=stream)
+
+    def new_token_kv(self, seed=0):
+        """One new token's K and V per sequence (device, the cache dtype)."""
+        g = torch.Generator(device="cuda")
+        g.manual_seed(int(seed))
+        shape = (self.B, self.hkv, self.D)
+        dt = TORCH_DT[self.cfg.dtype]
+        return (torch.randn(shape, generator=g, device="cuda").to(dt),
+                torch.randn(shape, generator=g, device="cuda").to(dt))
 
     def attention(self, l, out, table=None, stream=None):
         ema.paged_decode_attention(self.h, self.q, self.attn_dev[l] if table is None else table,
@@ -206,11 +234,15 @@ class StepRunner:
     the copy stream while attention of layer l runs on the attention stream
     (``mode="serial"``: one stream, copy then attention). Staging slot l % 2 is
     refilled only after the attention that last read it; attention of layer l
-    waits for its own prefetch. ``timers`` (optional) receives per-layer event
-    pairs: {"pf": [(start, end)] * L, "at": [(start, end)] * L}."""
+    waits for its own prefetch. With ``append``, each layer first stores the
+    new token's K/V (into the staged copy where the block is in the slice) and
+    the modified staged copies are written back on the copy stream after the
+    layer's attention, before the slot is refilled. ``timers`` (optional)
+    receives per-layer event pairs: {"pf": [(start, end)] * L, "at": [...]}."""
 
-    def __init__(self, w, mode="overlap"):
+    def __init__(self, w, mode="overlap", append=False):
         self.w = w
+        self.kv_new = w.new_token_kv() if append else None
         self.s1 = torch.cuda.Stream()
         self.s2 = torch.cuda.Stream() if mode == "overlap" else self.s1
         self.ev_pf = [torch.cuda.Event() for _ in range(w.L)]
@@ -243,12 +275,17 @@ class StepRunner:
                     s2.wait_event(self.ev_at[l - 1])   # slot (l+1) % 2 was read by layer l-1
                 self._prefetch(l + 1, timers)
             s1.wait_event(self.ev_pf[l])
+            if self.kv_new is not None:
+                w.append(l, *self.kv_new, stream=s1)
             if timers:
                 timers["at"][l][0].record(s1)
             w.attention(l, out, stream=s1)
             if timers:
                 timers["at"][l][1].record(s1)
             self.ev_at[l].record(s1)
+            if self.kv_new is not None:
+                s2.wait_event(self.ev_at[l])
+                w.writeback(l, stream=s2)
 
 
 class BlockedTimer:

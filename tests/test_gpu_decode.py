@@ -207,3 +207,35 @@ def test_decode_steps_with_append_and_writeback_match_oracle(ema, layout):
         print(f"max rel err {max(errs):.2e} over {len(errs)} layer-steps", flush=True)
     finally:
         w.close()
+
+
+@pytest.mark.parametrize("layout", [0, 1])
+def test_step_runner_append_reaches_every_block(ema, layout):
+    """The overlapped step with append: after one step every sequence's last
+    block, in every layer, holds the new token's K/V at its row -- read from the
+    slice block itself where the block lives in the slice (written back)."""
+    from harness import StepRunner
+    cfg = synth.LLAMA8B.scaled(layers=4, batch=5)
+    w = Workload(cfg, layers=4, lens=[1, 16, 17, 40, 95], slice_layout=layout, fill="device",
+                 frac=0.5)
+    try:
+        runner = StepRunner(w, "overlap", append=True)
+        out = w.new_out()
+        runner.run(out)
+        torch.cuda.synchronize()
+        k_new, v_new = (t.view(torch.int16).cpu().numpy().view(np.uint16) for t in runner.kv_new)
+        for l in range(w.L):
+            for b in range(w.B):
+                p = int(w.lens[b]) - 1
+                u = int(w.tables[l, b, p // w.bs])
+                if u >= w.n_local:
+                    blk, lay = w.slice_view[u - w.n_local].cpu().numpy(), layout
+                else:
+                    blk, lay = w.local_view[u].cpu().numpy(), synth.LAYOUT_ATTN
+                K, V = synth.unpack_block(blk, lay, w.hkv, w.bs, w.D)
+                assert np.array_equal(K[:, p % w.bs], k_new[b]), (l, b)
+                assert np.array_equal(V[:, p % w.bs], v_new[b]), (l, b)
+        assert sum(len(s) for s in w.wb_src) > 0          # some blocks were written back
+        assert ema.slice_device_errors(w.h) == 0
+    finally:
+        w.close()
