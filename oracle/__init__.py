@@ -30,11 +30,12 @@ from .slice_state import (SliceOracle, OracleError, FREE, STAGING, LENDER, LOCAL
                           ERR_INVAL, ERR_NOMEM, ERR_OWNER)
 from .attention import paged_decode_attention, contiguous_decode_attention
 from .invariants import check_ownership, check_conservation, check_sd_symmetry, logical_view
+from .sched import SchedOracle
 
 __all__ = [
     "LAYOUT_ATTN", "LAYOUT_NHD", "block_bytes", "decode_block", "encode_block", "convert_block",
     "to_float64", "SliceOracle", "OracleError", "FREE", "STAGING", "LENDER", "LOCAL", "SLICE",
     "ERR_INVAL", "ERR_NOMEM", "ERR_OWNER", "paged_decode_attention",
     "contiguous_decode_attention", "check_ownership", "check_conservation",
-    "check_sd_symmetry", "logical_view",
+    "check_sd_symmetry", "logical_view", "SchedOracle",
 ]
