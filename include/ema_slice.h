@@ -266,6 +266,40 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
  */
 int ema_slice_device_errors(ema_slice_t h, int32_t* count);
 
+/*
+ * Slice scheduling across GPUs (section 5.2, Appendix C) and bursty
+ * preemption control (section 5.3) -- host policy, no device work.
+ *
+ * n_gpus GPUs share one slice per unordered pair {i, j}, each of slice_units
+ * units. A request owned by GPU i places its units one at a time on a slice
+ * {i, j}, j != i, by Greedy-Least-Loaded: the incident slice with the lowest
+ * total use (both users' units; ties: the lowest j) among those with a free
+ * unit and, if GPU i is capped on it, below its cap. Releases free the
+ * request's most recently placed units first. A preemption of GPU i on slice
+ * {i, j} recorded while i holds more than half of the slice caps i's units
+ * there at that level for cap_window ticks; another such preemption within
+ * the window restarts it and lowers the cap if its level is lower; the cap
+ * lifts when a window passes without one. cap_window 0 disables caps.
+ * Handles are not thread-safe. Errors: INVAL (ranges, unknown request, more
+ * units released than held), NOMEM.
+ */
+typedef struct ema_sched* ema_sched_t;
+int ema_sched_create(int32_t n_gpus, int32_t slice_units, int64_t cap_window, ema_sched_t* out);
+int ema_sched_destroy(ema_sched_t s);
+/* Places n units of request `req` (any id >= 0) of GPU `gpu` at tick t:
+ * out_peer[n] (host) gets the peer j of each unit's slice, or -1 when no
+ * incident slice can take it; *placed (host, may be NULL) the number placed. */
+int ema_sched_place(ema_sched_t s, int32_t gpu, int32_t req, int32_t n, int64_t t,
+                    int32_t* out_peer, int32_t* placed);
+/* Releases n units of request `req` of GPU `gpu`, most recent first. */
+int ema_sched_release(ema_sched_t s, int32_t gpu, int32_t req, int32_t n);
+/* Records a preemption of GPU `gpu` on slice {gpu, peer} at tick t. */
+int ema_sched_preempted(ema_sched_t s, int32_t gpu, int32_t peer, int64_t t);
+/* use[n_gpus * n_gpus] (host): use[i * n_gpus + j] = units GPU i holds on
+ * slice {i, j}; cap[n_gpus * n_gpus] (host, may be NULL): GPU i's cap on that
+ * slice at tick t, or -1 when none is active. */
+int ema_sched_usage(ema_sched_t s, int64_t t, int32_t* use, int32_t* cap);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char* ema_last_error(void);
 

@@ -52,6 +52,16 @@ int fail(int code, const std::string& msg) {
   return code;
 }
 
+}  // namespace
+
+namespace ema {
+// Records the message behind an error code for ema_last_error (used by the
+// scheduler's entry points too).
+int set_error(int code, const std::string& msg) { return fail(code, msg); }
+}  // namespace ema
+
+namespace {
+
 int hip_fail(hipError_t e, const char* what) {
   return fail(EMA_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }

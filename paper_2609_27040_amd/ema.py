@@ -69,6 +69,12 @@ def _load():
         "ema_slice_reclaim": [P, I32, P, I64, P, ctypes.POINTER(ReclaimResult), P, I32, P, P, I32],
         "ema_paged_decode_attention": [P, P, P, P, I32, I32, I32, ctypes.c_float, P, P],
         "ema_slice_device_errors": [P, ctypes.POINTER(I32)],
+        "ema_sched_create": [I32, I32, I64, ctypes.POINTER(P)],
+        "ema_sched_destroy": [P],
+        "ema_sched_place": [P, I32, I32, I32, I64, P, ctypes.POINTER(I32)],
+        "ema_sched_release": [P, I32, I32, I32],
+        "ema_sched_preempted": [P, I32, I32, I64],
+        "ema_sched_usage": [P, I64, P, P],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -236,6 +242,69 @@ def slice_device_errors(h):
     c = ctypes.c_int32()
     _check(_lib.ema_slice_device_errors(h, ctypes.byref(c)))
     return c.value
+
+
+# ---- slice scheduling across GPUs (host policy) -------------------------------------
+
+def sched_create(n_gpus, slice_units, cap_window=0):
+    h = ctypes.c_void_p()
+    _check(_lib.ema_sched_create(int(n_gpus), int(slice_units), int(cap_window), ctypes.byref(h)))
+    return h.value
+
+
+def sched_destroy(s):
+    _check(_lib.ema_sched_destroy(s))
+
+
+def sched_place(s, gpu, req, n, t=0):
+    """Peers of the slices the n units went to (-1: refused)."""
+    peers = np.empty(max(int(n), 1), dtype=np.int32)
+    placed = ctypes.c_int32()
+    _check(_lib.ema_sched_place(s, int(gpu), int(req), int(n), int(t), peers.ctypes.data,
+                                ctypes.byref(placed)))
+    return peers[:int(n)].tolist()
+
+
+def sched_release(s, gpu, req, n):
+    _check(_lib.ema_sched_release(s, int(gpu), int(req), int(n)))
+
+
+def sched_preempted(s, gpu, peer, t):
+    _check(_lib.ema_sched_preempted(s, int(gpu), int(peer), int(t)))
+
+
+def sched_usage(s, m, t=0):
+    """(use, cap) as int arrays [m][m]; cap -1 where none is active."""
+    use = np.empty(m * m, dtype=np.int32)
+    cap = np.empty(m * m, dtype=np.int32)
+    _check(_lib.ema_sched_usage(s, int(t), use.ctypes.data, cap.ctypes.data))
+    return use.reshape(m, m), cap.reshape(m, m)
+
+
+class Scheduler:
+    """Greedy-Least-Loaded placement over the slices of n_gpus GPUs, with
+    bursty preemption caps (the sched_* calls on one handle)."""
+
+    def __init__(self, n_gpus, slice_units, cap_window=0):
+        self.m = int(n_gpus)
+        self.h = sched_create(n_gpus, slice_units, cap_window)
+
+    def place(self, gpu, req, n, t=0):
+        return sched_place(self.h, gpu, req, n, t)
+
+    def release(self, gpu, req, n):
+        sched_release(self.h, gpu, req, n)
+
+    def preempted(self, gpu, peer, t):
+        sched_preempted(self.h, gpu, peer, t)
+
+    def usage(self, t=0):
+        return sched_usage(self.h, self.m, t)
+
+    def close(self):
+        if self.h:
+            sched_destroy(self.h)
+            self.h = None
 
 
 # ---- plumbing: library-owned pools as torch tensors ---------------------------------
