@@ -56,7 +56,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama3-8b-kv",
-                    choices=["llama3-8b-kv", "llama-70b-tp8-share", "bursty-8b", "stress"])
+                    choices=["llama3-8b-kv", "llama-70b-tp8-share", "bursty-8b", "stress",
+                             "slab-sweep"])
     ap.add_argument("--mode", default="overlap", choices=["overlap", "serial"])
     ap.add_argument("--append", action="store_true",
                     help="each layer also appends the new token's K/V and writes the modified "
@@ -335,6 +336,32 @@ def stress_main(args):
     print(json.dumps(res))
 
 
+def slab_main(args):
+    """Copy efficiency against transfer size: prefetch of every slice block of a
+    block-size-16 pool (8 GiB, 60 % slice) as contiguous runs of 1 to 400
+    blocks, by the gather kernel and by the copy engines; one JSON line."""
+    import torch
+    from stress import run_sweep
+
+    torch.cuda.set_device(0)
+    log("slab sweep")
+    rows = run_sweep()
+    if not all(r["exact"] for r in rows):
+        raise RuntimeError("sampled copies differ")
+    best = max(r["kernel"]["GBps"] for r in rows)
+    res = {"metric": "prefetch/reclaim GB/s + paged decode tokens/s, % of HBM roofline, 1 GPU",
+           "value": best, "unit": "GB/s", "n_gpus": 1, "steps": 1, "warmup": 0,
+           "ms_per_step": None, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "f16", "data": "synthetic",
+           "config": {"workload": "slab-sweep", "block_size": 16, "kv_heads": 8,
+                      "blocks": 1 << 17, "slice_frac": 0.6},
+           "sweep": rows}
+    for r in rows:
+        log(f"run {r['run_blocks']:4d} blocks: kernel {r['kernel']['GBps']:.0f} GB/s, "
+            f"copy engines {r['dma']['GBps']:.0f} GB/s (end to end {r['dma']['wall_GBps']:.0f})")
+    print(json.dumps(res))
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -349,6 +376,9 @@ def main():
         return
     if args.workload == "stress":
         stress_main(args)
+        return
+    if args.workload == "slab-sweep":
+        slab_main(args)
         return
     import torch
     import synth

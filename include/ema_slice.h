@@ -168,6 +168,29 @@ int ema_slice_lend(ema_slice_t h, int32_t n_blocks, int32_t* added);
 int ema_slice_prefetch(ema_slice_t h, const int32_t* block_ids, const int32_t* dst_block_table,
                        int32_t n, void* stream);
 
+#define EMA_ENGINE_KERNEL 0  /* copy runs with the gather kernel (compute units)      */
+#define EMA_ENGINE_DMA 1     /* copy runs with the copy engines, one transfer per run */
+
+/*
+ * slice_prefetch_runs -- prefetch of contiguous runs (section 4.2: the slab and
+ * layer-group layouts keep a user's data physically contiguous so that a swap
+ * is a few large transfers). For r < n_runs: the run_blocks[r] local blocks
+ * from dst_first[r] <- the slice blocks from src_first[r], i.e. block
+ * dst_first[r] + k <- block src_first[r] + k for k < run_blocks[r] (unified
+ * ids; host arrays, so the call can issue one transfer per run). Sources must
+ * be owned slice blocks, destinations EMA_STAGING local blocks, no block named
+ * twice. engine EMA_ENGINE_KERNEL expands the runs into one block list for the
+ * gather kernel (any slice layout); EMA_ENGINE_DMA issues one device-to-device
+ * transfer per run on the copy engines, leaving the compute units free (slice
+ * in EMA_LAYOUT_ATTN only: the engines copy bytes as they are). The list
+ * upload shares the reclaim plan buffer and first waits for its previous
+ * upload. Async on `stream`. Errors: INVAL (validated on the host in every
+ * mode), HIP.
+ */
+int ema_slice_prefetch_runs(ema_slice_t h, const int32_t* src_first, const int32_t* dst_first,
+                            const int32_t* run_blocks, int32_t n_runs, int32_t engine,
+                            void* stream);
+
 /*
  * Moves logical blocks between pools: block dst_ids[i] <- block src_ids[i]
  * (device [n] unified ids; each destination already allocated to the

@@ -9,6 +9,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
@@ -296,6 +297,63 @@ int ema_slice_prefetch(ema_slice_t h, const int32_t* block_ids, const int32_t* d
 int ema_slice_migrate(ema_slice_t h, const int32_t* src_ids, const int32_t* dst_ids, int32_t n,
                       void* stream) {
   return copy_entry(h, src_ids, dst_ids, n, stream, CopyKind::kMigrate);
+}
+
+int ema_slice_prefetch_runs(ema_slice_t h, const int32_t* src_first, const int32_t* dst_first,
+                            const int32_t* run_blocks, int32_t n_runs, int32_t engine,
+                            void* stream) {
+  if (!h) return fail(EMA_ERR_INVAL, "prefetch_runs: NULL handle");
+  if (n_runs < 0 || (n_runs > 0 && (!src_first || !dst_first || !run_blocks)))
+    return fail(EMA_ERR_INVAL, "prefetch_runs: n_runs < 0 or NULL array");
+  if (engine != EMA_ENGINE_KERNEL && engine != EMA_ENGINE_DMA)
+    return fail(EMA_ERR_INVAL, "prefetch_runs: unknown engine");
+  if (engine == EMA_ENGINE_DMA && h->shape.slice_layout != EMA_LAYOUT_ATTN)
+    return fail(EMA_ERR_INVAL, "prefetch_runs: the copy engines need the slice in the local layout");
+  const int64_t n_total = int64_t(h->book.n_local()) + h->book.n_slice();
+  std::vector<int32_t> src, dst;
+  for (int32_t r = 0; r < n_runs; ++r) {
+    const int64_t a = src_first[r], b = dst_first[r], k = run_blocks[r];
+    if (k < 0 || a < 0 || b < 0 || a + k > n_total || b + k > n_total ||
+        int64_t(src.size()) + k > n_total)
+      return fail(EMA_ERR_INVAL, "prefetch_runs: run out of range");
+    for (int64_t i = 0; i < k; ++i) {
+      src.push_back(int32_t(a + i));
+      dst.push_back(int32_t(b + i));
+    }
+  }
+  const int32_t n = int32_t(src.size());
+  std::string err;
+  int rc = h->book.check_prefetch(src.data(), dst.data(), n, &err);
+  if (rc) return fail(rc, err);
+  if (h->host_only || n == 0) return EMA_OK;
+  if ((rc = use_device(h))) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (engine == EMA_ENGINE_DMA) {
+    const ema::PoolView pv = pool_view(h);
+    for (int32_t r = 0; r < n_runs; ++r) {
+      if (run_blocks[r] == 0) continue;
+      char* d = pv.local + int64_t(dst_first[r]) * h->bb;
+      const char* sp = pv.slice + (int64_t(src_first[r]) - pv.n_local) * h->bb;
+      HIP_TRY(hipMemcpyAsync(d, sp, size_t(run_blocks[r]) * h->bb, hipMemcpyDeviceToDeviceNoCU, st),
+              "prefetch_runs copy");
+    }
+    return EMA_OK;
+  }
+  if (h->h_work_pending) {
+    HIP_TRY(hipEventSynchronize(h->h_work_ev), "hipEventSynchronize(runs)");
+    h->h_work_pending = false;
+  }
+  if (size_t(2) * n > h->h_work_cap || size_t(2) * n > h->work_cap)
+    return fail(EMA_ERR_INVAL, "prefetch_runs: more blocks than the plan buffer holds");
+  std::copy(src.begin(), src.end(), h->h_work);
+  std::copy(dst.begin(), dst.end(), h->h_work + n);
+  HIP_TRY(hipMemcpyAsync(h->d_work, h->h_work, size_t(2) * n * 4, hipMemcpyHostToDevice, st),
+          "hipMemcpyAsync(runs)");
+  HIP_TRY(hipEventRecord(h->h_work_ev, st), "hipEventRecord(runs)");
+  h->h_work_pending = true;
+  HIP_TRY(ema::launch_block_copy(pool_view(h), h->d_work, h->d_work + n, n, h->d_err, st),
+          "prefetch_runs launch");
+  return EMA_OK;
 }
 
 int ema_slice_writeback(ema_slice_t h, const int32_t* staging_ids, const int32_t* slice_ids,

@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "libe
 OK, ERR_INVAL, ERR_NOMEM, ERR_OWNER, ERR_HIP = 0, -1, -2, -3, -4
 F16, BF16 = 0, 1
 LAYOUT_ATTN, LAYOUT_NHD = 0, 1
+ENGINE_KERNEL, ENGINE_DMA = 0, 1
 POOL_LOCAL, POOL_SLICE = 0, 1
 FREE, STAGING, LENDER = -1, -2, -3
 CREATE_HOST_ONLY, CREATE_CHECKED = 1, 2
@@ -65,6 +66,7 @@ def _load():
         "ema_slice_prefetch": [P, P, P, I32, P],
         "ema_slice_migrate": [P, P, P, I32, P],
         "ema_slice_writeback": [P, P, P, I32, P],
+        "ema_slice_prefetch_runs": [P, P, P, P, I32, I32, P],
         "ema_kv_append": [P, P, P, P, P, I32, I32, P],
         "ema_slice_reclaim": [P, I32, P, I64, P, ctypes.POINTER(ReclaimResult), P, I32, P, P, I32],
         "ema_paged_decode_attention": [P, P, P, P, I32, I32, I32, ctypes.c_float, P, P],
@@ -181,6 +183,15 @@ def slice_migrate(h, src_ids, dst_ids, n=None, stream=None):
         src_ids, dst_ids = _i32_host(src_ids), _i32_host(dst_ids)
     _check(_lib.ema_slice_migrate(h, _ptr(src_ids), _ptr(dst_ids), int(n),
                                   None if host else _stream(stream)))
+
+
+def slice_prefetch_runs(h, src_first, dst_first, run_blocks, engine=0, stream=None):
+    """Contiguous runs (host int arrays); engine ENGINE_KERNEL or ENGINE_DMA."""
+    src_first, dst_first, run_blocks = (_i32_host(a) for a in (src_first, dst_first, run_blocks))
+    info_host = slice_get_info(h)["device"] < 0
+    _check(_lib.ema_slice_prefetch_runs(h, src_first.ctypes.data, dst_first.ctypes.data,
+                                        run_blocks.ctypes.data, len(run_blocks), int(engine),
+                                        None if info_host else _stream(stream)))
 
 
 def slice_writeback(h, staging_ids, slice_ids, n=None, stream=None):

@@ -155,3 +155,51 @@ class StressRun:
     def close(self):
         self.timer.close()
         self.w.close()
+
+
+RUN_BLOCKS = (1, 4, 16, 64, 100, 200, 400)
+
+
+def run_sweep(bs=16, n_blocks=1 << 17, run_blocks=RUN_BLOCKS, reps=3):
+    """Prefetch of every slice block as contiguous runs of R blocks (the slab x
+    layer-group chunks of a layer-group-major slice), by the gather kernel and
+    by the copy engines. Slice slots are taken in order (every slot is owned:
+    the slice is exactly full) into the contiguous staging area. Returns, per
+    R, device GB/s (events behind a blocking copy) and end-to-end GB/s (host
+    submission included: one transfer per run for the copy engines)."""
+    import time
+    run = StressRun(bs, n_blocks=n_blocks)
+    w = run.w
+    try:
+        n = len(w.pf_src[0])
+        s0, d0 = w.n_local, int(w.staging[0, 0])
+        out = []
+        for R in run_blocks:
+            k = n // R
+            src_first = s0 + R * np.arange(k)
+            dst_first = d0 + R * np.arange(k)
+            runs = np.full(k, R)
+            nbytes = 2 * k * R * w.bb
+            rec = {"run_blocks": R, "run_bytes": R * w.bb, "runs": int(k)}
+            for name, eng in (("kernel", ema.ENGINE_KERNEL), ("dma", ema.ENGINE_DMA)):
+                call = lambda: ema.slice_prefetch_runs(w.h, src_first, dst_first, runs, eng,
+                                                       stream=run.s)
+                dev, wall = [], []
+                for _ in range(reps):
+                    _, ms, host_ms, covered = run.timer.time(run.s, call, host_ms=2.0 + k * 0.02)
+                    dev.append(ms)
+                    torch.cuda.synchronize()
+                    t0 = time.perf_counter()
+                    call()
+                    torch.cuda.synchronize()
+                    wall.append((time.perf_counter() - t0) * 1e3)
+                rec[name] = {"GBps": nbytes / (np.median(dev) / 1e3) / 1e9,
+                             "wall_GBps": nbytes / (np.median(wall) / 1e3) / 1e9,
+                             "device_only": bool(covered)}
+            pick = run._sample(k * R)
+            ok = np.array_equal(run._rows(s0 + pick), run._rows(d0 + pick))
+            rec["exact"] = bool(ok)
+            out.append(rec)
+        return out
+    finally:
+        run.close()

@@ -211,3 +211,45 @@ def test_reclaim_with_writeback_and_preemption_large(ema):
         oracle.check_ownership(st, cache.tables)
     finally:
         gpu.close()
+
+
+@pytest.mark.parametrize("engine", [0, 1])
+def test_prefetch_runs_match_oracle_bit_for_bit(ema, engine):
+    """Contiguous runs copied by the gather kernel or the copy engines give the
+    same bytes as the oracle's block-by-block prefetch (runs of 1, 3 and 5)."""
+    gpu, st = make_pair(ema, 16, 0, "bf16", 30, 20, seed=40 + engine, hkv=2)
+    try:
+        owners = np.arange(20) % 4
+        gpu.alloc_blocks(1, owners)
+        st.alloc_blocks(1, owners)
+        dst = gpu.alloc_blocks(0, [-2] * 12)
+        st.alloc_blocks(0, [-2] * 12)
+        nl = st.n_local
+        src_first = np.array([nl + 2, nl + 9, nl + 15])
+        dst_first = np.array([dst[0], dst[1], dst[4]])
+        runs = np.array([1, 3, 5])
+        ema.slice_prefetch_runs(gpu.h, src_first, dst_first, runs, engine=engine)
+        for a, b, k in zip(src_first, dst_first, runs):
+            st.prefetch(list(range(a, a + k)), list(range(b, b + k)))
+        assert_pools_equal(gpu, st)
+    finally:
+        gpu.close()
+
+
+def test_prefetch_runs_validation(ema):
+    gpu, st = make_pair(ema, 16, 1, "bf16", 12, 8, seed=44)
+    try:
+        gpu.alloc_blocks(1, [0] * 8)
+        dst = gpu.alloc_blocks(0, [-2] * 4)
+        nl = 12
+        cases = [([nl], [dst[0]], [2], 1),            # copy engines need the local layout
+                 ([nl], [dst[0]], [9], 0),            # run past the pool
+                 ([nl, nl + 1], [dst[0], dst[0]], [1, 1], 0),   # a staging block twice
+                 ([0], [dst[0]], [1], 0)]             # source not a slice block
+        for s, d, k, eng in cases:
+            with pytest.raises(ema.EmaError) as e:
+                ema.slice_prefetch_runs(gpu.h, s, d, k, engine=eng)
+            assert e.value.code == ema.ERR_INVAL
+        assert_pools_equal(gpu, st)
+    finally:
+        gpu.close()
