@@ -27,8 +27,10 @@
  *
  * Conventions
  *   Return value: EMA_OK or a negative EMA_ERR_*; ema_last_error() gives a
- *   message (thread-local). Host bookkeeping is all-or-nothing: on error no
- *   state changes.
+ *   message (thread-local). No C++ exception leaves the library. Host
+ *   bookkeeping is all-or-nothing: on error no state changes, except that a
+ *   HIP error raised after a call's bookkeeping took effect (reclaim; see
+ *   there) leaves that bookkeeping in place.
  *   Pointers marked "device" are HIP device pointers owned by the caller;
  *   "host" pointers are ordinary memory. The library owns both pools.
  *   `stream` is a hipStream_t (NULL = the null stream). Kernels are enqueued
@@ -55,7 +57,8 @@ extern "C" {
 
 #define EMA_OK 0
 #define EMA_ERR_INVAL (-1)   /* bad argument, range, duplicate, wrong tag  */
-#define EMA_ERR_NOMEM (-2)   /* not enough free blocks (slice: below lim)  */
+#define EMA_ERR_NOMEM (-2)   /* not enough free blocks (slice: below lim),
+                                or host memory exhausted                   */
 #define EMA_ERR_OWNER (-3)   /* freeing a block that is not allocated      */
 #define EMA_ERR_HIP (-4)     /* a HIP runtime call failed                  */
 
@@ -253,9 +256,13 @@ int ema_kv_append(ema_slice_t h, const void* k_new, const void* v_new, const int
  * NULL): the copies made. Counts beyond a cap are still reported in result.
  * In host-only mode canon_tables must be NULL with n_entries 0.
  * The plan (8 bytes per moved or released block) is uploaded from the
- * handle's pinned buffer; a reclaim first waits for the previous reclaim's
- * upload to finish, never for anything else on the device.
- * Errors: INVAL (n_blocks < 0, n_entries < 0, bad table pointer), HIP.
+ * handle's pinned buffer; a reclaim first waits for the previous upload from
+ * that buffer (a reclaim's, or a kernel-engine run prefetch's) to finish,
+ * never for anything else on the device.
+ * Errors: INVAL (n_blocks < 0, n_entries < 0, bad table pointer), HIP. The
+ * bookkeeping changes before the copies are enqueued: after a HIP error the
+ * ownership and lim already reflect the plan, while the copies and the table
+ * rewrite may not have run.
  */
 int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, int64_t n_entries,
                       void* stream, ema_reclaim_result* result, int32_t* victims,
@@ -304,7 +311,7 @@ int ema_slice_device_errors(ema_slice_t h, int32_t* count);
  * the window restarts it and lowers the cap if its level is lower; the cap
  * lifts when a window passes without one. cap_window 0 disables caps.
  * Handles are not thread-safe. Errors: INVAL (ranges, unknown request, more
- * units released than held), NOMEM.
+ * units released than held), NOMEM (host memory).
  */
 typedef struct ema_sched* ema_sched_t;
 int ema_sched_create(int32_t n_gpus, int32_t slice_units, int64_t cap_window, ema_sched_t* out);

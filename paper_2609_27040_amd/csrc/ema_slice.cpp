@@ -13,6 +13,8 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <exception>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -59,7 +61,23 @@ namespace ema {
 // Records the message behind an error code for ema_last_error (used by the
 // scheduler's entry points too).
 int set_error(int code, const std::string& msg) { return fail(code, msg); }
+
+// Called from the catch handler of every entry point: no C++ exception
+// crosses the C ABI; host allocation failures become EMA_ERR_NOMEM.
+int internal_error() {
+  try {
+    throw;
+  } catch (const std::bad_alloc&) {
+    return fail(EMA_ERR_NOMEM, "out of host memory");
+  } catch (const std::exception& e) {
+    return fail(EMA_ERR_INVAL, std::string("internal error: ") + e.what());
+  } catch (...) {
+    return fail(EMA_ERR_INVAL, "internal error");
+  }
+}
 }  // namespace ema
+
+using ema::internal_error;
 
 namespace {
 
@@ -142,7 +160,7 @@ extern "C" {
 const char* ema_last_error(void) { return g_err.c_str(); }
 
 int ema_slice_create(const ema_kv_shape* shape, size_t local_bytes, size_t lent_bytes,
-                     uint32_t flags, ema_slice_t* out) {
+                     uint32_t flags, ema_slice_t* out) try {
   if (!shape || !out) return fail(EMA_ERR_INVAL, "create: NULL argument");
   *out = nullptr;
   if (shape->num_kv_heads < 1 || shape->num_kv_heads > 64 || shape->head_dim != 128 ||
@@ -194,9 +212,11 @@ int ema_slice_create(const ema_kv_shape* shape, size_t local_bytes, size_t lent_
   }
   *out = h;
   return EMA_OK;
+} catch (...) {
+  return internal_error();
 }
 
-int ema_slice_destroy(ema_slice_t h) {
+int ema_slice_destroy(ema_slice_t h) try {
   if (!h) return fail(EMA_ERR_INVAL, "destroy: NULL handle");
   if (!h->host_only) {
     int rc = use_device(h);
@@ -204,9 +224,11 @@ int ema_slice_destroy(ema_slice_t h) {
   }
   release(h);
   return EMA_OK;
+} catch (...) {
+  return internal_error();
 }
 
-int ema_slice_get_info(ema_slice_t h, ema_slice_info* out) {
+int ema_slice_get_info(ema_slice_t h, ema_slice_info* out) try {
   if (!h || !out) return fail(EMA_ERR_INVAL, "info: NULL argument");
   out->block_bytes = h->bb;
   out->n_local = h->book.n_local();
@@ -218,37 +240,47 @@ int ema_slice_get_info(ema_slice_t h, ema_slice_info* out) {
   out->local_base = h->local;
   out->slice_base = h->slice;
   return EMA_OK;
+} catch (...) {
+  return internal_error();
 }
 
-int ema_slice_owners(ema_slice_t h, int32_t* own_local, int32_t* own_slice) {
+int ema_slice_owners(ema_slice_t h, int32_t* own_local, int32_t* own_slice) try {
   if (!h) return fail(EMA_ERR_INVAL, "owners: NULL handle");
   if (own_local && h->book.n_local())
     std::memcpy(own_local, h->book.own_local().data(), size_t(h->book.n_local()) * 4);
   if (own_slice && h->book.n_slice())
     std::memcpy(own_slice, h->book.own_slice().data(), size_t(h->book.n_slice()) * 4);
   return EMA_OK;
+} catch (...) {
+  return internal_error();
 }
 
 int ema_slice_alloc_blocks(ema_slice_t h, int32_t pool, int32_t n, const int32_t* owners,
-                           int32_t* out_ids) {
+                           int32_t* out_ids) try {
   if (!h) return fail(EMA_ERR_INVAL, "alloc: NULL handle");
   std::string err;
   const int rc = h->book.alloc(pool, n, owners, out_ids, &err);
   return rc ? fail(rc, err) : EMA_OK;
+} catch (...) {
+  return internal_error();
 }
 
-int ema_slice_free_blocks(ema_slice_t h, const int32_t* ids, int32_t n) {
+int ema_slice_free_blocks(ema_slice_t h, const int32_t* ids, int32_t n) try {
   if (!h) return fail(EMA_ERR_INVAL, "free: NULL handle");
   std::string err;
   const int rc = h->book.free_blocks(ids, n, &err);
   return rc ? fail(rc, err) : EMA_OK;
+} catch (...) {
+  return internal_error();
 }
 
-int ema_slice_lend(ema_slice_t h, int32_t n_blocks, int32_t* added) {
+int ema_slice_lend(ema_slice_t h, int32_t n_blocks, int32_t* added) try {
   if (!h) return fail(EMA_ERR_INVAL, "lend: NULL handle");
   std::string err;
   const int rc = h->book.lend(n_blocks, added, &err);
   return rc ? fail(rc, err) : EMA_OK;
+} catch (...) {
+  return internal_error();
 }
 
 enum class CopyKind { kPrefetch, kMigrate, kWriteback };
@@ -290,18 +322,22 @@ static int copy_entry(ema_slice_t h, const int32_t* src, const int32_t* dst, int
 }
 
 int ema_slice_prefetch(ema_slice_t h, const int32_t* block_ids, const int32_t* dst_block_table,
-                       int32_t n, void* stream) {
+                       int32_t n, void* stream) try {
   return copy_entry(h, block_ids, dst_block_table, n, stream, CopyKind::kPrefetch);
+} catch (...) {
+  return internal_error();
 }
 
 int ema_slice_migrate(ema_slice_t h, const int32_t* src_ids, const int32_t* dst_ids, int32_t n,
-                      void* stream) {
+                      void* stream) try {
   return copy_entry(h, src_ids, dst_ids, n, stream, CopyKind::kMigrate);
+} catch (...) {
+  return internal_error();
 }
 
 int ema_slice_prefetch_runs(ema_slice_t h, const int32_t* src_first, const int32_t* dst_first,
                             const int32_t* run_blocks, int32_t n_runs, int32_t engine,
-                            void* stream) {
+                            void* stream) try {
   if (!h) return fail(EMA_ERR_INVAL, "prefetch_runs: NULL handle");
   if (n_runs < 0 || (n_runs > 0 && (!src_first || !dst_first || !run_blocks)))
     return fail(EMA_ERR_INVAL, "prefetch_runs: n_runs < 0 or NULL array");
@@ -354,15 +390,19 @@ int ema_slice_prefetch_runs(ema_slice_t h, const int32_t* src_first, const int32
   HIP_TRY(ema::launch_block_copy(pool_view(h), h->d_work, h->d_work + n, n, h->d_err, st),
           "prefetch_runs launch");
   return EMA_OK;
+} catch (...) {
+  return internal_error();
 }
 
 int ema_slice_writeback(ema_slice_t h, const int32_t* staging_ids, const int32_t* slice_ids,
-                        int32_t n, void* stream) {
+                        int32_t n, void* stream) try {
   return copy_entry(h, staging_ids, slice_ids, n, stream, CopyKind::kWriteback);
+} catch (...) {
+  return internal_error();
 }
 
 int ema_kv_append(ema_slice_t h, const void* k_new, const void* v_new, const int32_t* block_table,
-                  const int32_t* seq_lens, int32_t batch, int32_t max_blocks, void* stream) {
+                  const int32_t* seq_lens, int32_t batch, int32_t max_blocks, void* stream) try {
   if (!h) return fail(EMA_ERR_INVAL, "append: NULL handle");
   if (batch < 0 || max_blocks < 0) return fail(EMA_ERR_INVAL, "append: bad batch or max_blocks");
   if (batch > 0 && (!k_new || !v_new || !block_table || !seq_lens))
@@ -396,12 +436,14 @@ int ema_kv_append(ema_slice_t h, const void* k_new, const void* v_new, const int
                                 max_blocks, h->d_err, st),
           "append launch");
   return EMA_OK;
+} catch (...) {
+  return internal_error();
 }
 
 int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, int64_t n_entries,
                       void* stream, ema_reclaim_result* result, int32_t* victims,
                       int32_t victims_cap, int32_t* moves_src, int32_t* moves_dst,
-                      int32_t moves_cap) {
+                      int32_t moves_cap) try {
   if (!h || !result) return fail(EMA_ERR_INVAL, "reclaim: NULL handle or result");
   if (n_blocks < 0 || n_entries < 0 || (n_entries > 0 && !canon_tables))
     return fail(EMA_ERR_INVAL, "reclaim: bad count or table pointer");
@@ -441,15 +483,10 @@ int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, in
     HIP_TRY(hipEventSynchronize(h->h_work_ev), "hipEventSynchronize(reclaim)");
     h->h_work_pending = false;
   }
-  if (need > h->h_work_cap) {
-    if (h->h_work) HIP_TRY(hipHostFree(h->h_work), "hipHostFree");
-    h->h_work = nullptr;
-    h->h_work_cap = 0;
-    HIP_TRY(hipHostMalloc(&h->h_work, (need + need / 4) * 4, hipHostMallocDefault),
-            "hipHostMalloc");
-    h->h_work_cap = need + need / 4;
-  }
-  if ((rc = grow_device(reinterpret_cast<void**>(&h->d_work), &h->work_cap, need, 4))) return rc;
+  // movers and released blocks are disjoint, so np <= n_total and the
+  // buffers sized at create always hold the plan
+  if (need > h->h_work_cap || need > h->work_cap)
+    return fail(EMA_ERR_INVAL, "reclaim: plan larger than the work buffers");
   int32_t* keys = h->h_work;
   int32_t* vals = h->h_work + np;
   for (int32_t i = 0; i < m; ++i) {
@@ -476,11 +513,13 @@ int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, in
     HIP_TRY(ema::launch_remap_scatter(h->d_remap, n_total, dkeys, dkeys, np, st), "remap reset");
   }
   return EMA_OK;
+} catch (...) {
+  return internal_error();
 }
 
 int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* block_table,
                                const int32_t* seq_lens, int32_t batch, int32_t num_q_heads,
-                               int32_t max_blocks, float scale, float* out, void* stream) {
+                               int32_t max_blocks, float scale, float* out, void* stream) try {
   if (!h) return fail(EMA_ERR_INVAL, "attention: NULL handle");
   const int32_t hkv = h->shape.num_kv_heads;
   if (batch < 0 || max_blocks < 0 || num_q_heads < hkv || num_q_heads % hkv != 0)
@@ -562,9 +601,11 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
                        : ema::launch_paged_attention_mfma(a, st),
           "attention launch");
   return EMA_OK;
+} catch (...) {
+  return internal_error();
 }
 
-int ema_slice_device_errors(ema_slice_t h, int32_t* count) {
+int ema_slice_device_errors(ema_slice_t h, int32_t* count) try {
   if (!h || !count) return fail(EMA_ERR_INVAL, "device_errors: NULL argument");
   *count = 0;
   if (h->host_only) return EMA_OK;
@@ -574,6 +615,8 @@ int ema_slice_device_errors(ema_slice_t h, int32_t* count) {
   HIP_TRY(hipMemcpy(count, h->d_err, 4, hipMemcpyDeviceToHost), "hipMemcpy(err)");
   HIP_TRY(hipMemset(h->d_err, 0, 4), "hipMemset(err)");
   return EMA_OK;
+} catch (...) {
+  return internal_error();
 }
 
 }  // extern "C"

@@ -2,7 +2,7 @@
 #include "slice_book.h"
 
 #include <algorithm>
-#include <unordered_map>
+#include <functional>
 #include <unordered_set>
 
 namespace ema {
@@ -244,22 +244,42 @@ int SliceBook::reclaim(int32_t n, ReclaimPlan* p, std::string* err) {
   p->reclaimed = ne;
   p->cut = cut;
 
+  // Every allocation comes before the first change of state, so a failed
+  // host allocation leaves the book as it was.
   std::vector<int32_t> movers;  // slice slots in [cut, lim) owned by a sequence
+  movers.reserve(size_t(ne));
   for (int32_t s = cut; s < lim_; ++s)
     if (own_slice_[s] >= 0) movers.push_back(s);
+  const size_t m0 = movers.size();
+  // Preempting an owner removes only its own movers, so the owners ranked
+  // once by (movers desc, id desc) give the order in which step 4 takes them.
+  std::vector<std::pair<int32_t, int32_t>> rank;   // (count, owner)
+  {
+    std::vector<int32_t> own(m0);
+    for (size_t i = 0; i < m0; ++i) own[i] = own_slice_[movers[i]];
+    std::sort(own.begin(), own.end());
+    rank.reserve(m0);
+    for (size_t i = 0; i < m0;) {
+      size_t j = i;
+      while (j < m0 && own[j] == own[i]) ++j;
+      rank.emplace_back(int32_t(j - i), own[i]);
+      i = j;
+    }
+    std::sort(rank.begin(), rank.end(), std::greater<std::pair<int32_t, int32_t>>());
+  }
+  std::vector<int32_t> dst(m0);
+  p->victims.reserve(rank.size());
+  p->victim_blocks.reserve(size_t(n_local_) + size_t(n_slice_));
+  p->move_src.reserve(m0);
+  p->move_dst.reserve(m0);
+
   auto n_dest = [&]() {
     return int64_t(free_slice_.count_below(cut)) + free_local_.count();
   };
-
-  while (int64_t(movers.size()) > n_dest()) {
-    std::unordered_map<int32_t, int32_t> cnt;
-    for (int32_t s : movers) ++cnt[own_slice_[s]];
-    int32_t best = -1, best_c = -1;
-    for (const auto& kv : cnt)
-      if (kv.second > best_c || (kv.second == best_c && kv.first > best)) {
-        best = kv.first;
-        best_c = kv.second;
-      }
+  int64_t alive = int64_t(m0);
+  for (size_t k = 0; alive > n_dest(); ++k) {
+    const int32_t best = rank[k].second;
+    alive -= rank[k].first;
     p->victims.push_back(best);
     for (int32_t u = 0; u < n_local_; ++u)
       if (own_local_[u] == best) {
@@ -271,25 +291,21 @@ int SliceBook::reclaim(int32_t n, ReclaimPlan* p, std::string* err) {
         p->victim_blocks.push_back(n_local_ + s);
         set_owner(n_local_ + s, kFree);
       }
+  }
+  if (!p->victims.empty())
     movers.erase(std::remove_if(movers.begin(), movers.end(),
                                 [&](int32_t s) { return own_slice_[s] < 0; }),
                  movers.end());
-  }
 
   const int32_t m = int32_t(movers.size());
-  std::vector<int32_t> dst(m);
   const int32_t got_s = free_slice_.lowest(m, cut, dst.data());
   for (int32_t i = 0; i < got_s; ++i) dst[i] += n_local_;
   const int32_t got_l = free_local_.lowest(m - got_s, n_local_, dst.data() + got_s);
-  if (got_s + got_l != m) {
-    *err = "reclaim: internal destination-count mismatch";
-    return kErrNomem;
-  }
-  p->move_src.resize(m);
-  p->move_dst = dst;
+  // got_s + got_l == m: the loop above stops only once m <= n_dest()
   for (int32_t i = 0; i < m; ++i) {
     const int32_t o = own_slice_[movers[i]];
-    p->move_src[i] = n_local_ + movers[i];
+    p->move_src.push_back(n_local_ + movers[i]);
+    p->move_dst.push_back(dst[i]);
     set_owner(dst[i], o);
   }
   p->written_back = got_l;

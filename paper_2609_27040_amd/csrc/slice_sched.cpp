@@ -11,6 +11,7 @@
 
 namespace ema {
 int set_error(int code, const std::string& msg);   // ema_slice.cpp
+int internal_error();                              // ema_slice.cpp, from a catch handler
 }
 
 struct ema_sched {
@@ -32,7 +33,7 @@ using ema::set_error;
 
 extern "C" {
 
-int ema_sched_create(int32_t n_gpus, int32_t slice_units, int64_t cap_window, ema_sched_t* out) {
+int ema_sched_create(int32_t n_gpus, int32_t slice_units, int64_t cap_window, ema_sched_t* out) try {
   if (!out) return set_error(EMA_ERR_INVAL, "sched_create: NULL out");
   *out = nullptr;
   if (n_gpus < 2 || n_gpus > 4096 || slice_units < 1 || cap_window < 0)
@@ -46,18 +47,30 @@ int ema_sched_create(int32_t n_gpus, int32_t slice_units, int64_t cap_window, em
   s->cap_until.assign(size_t(n_gpus) * n_gpus, 0);
   *out = s;
   return EMA_OK;
+} catch (...) {
+  return ema::internal_error();
 }
 
-int ema_sched_destroy(ema_sched_t s) {
+int ema_sched_destroy(ema_sched_t s) try {
   delete s;
   return EMA_OK;
+} catch (...) {
+  return ema::internal_error();
 }
 
 int ema_sched_place(ema_sched_t s, int32_t gpu, int32_t req, int32_t n, int64_t t,
-                    int32_t* out_peer, int32_t* placed) {
+                    int32_t* out_peer, int32_t* placed) try {
   if (!s || gpu < 0 || gpu >= s->m || req < 0 || n < 0 || (n > 0 && !out_peer))
     return set_error(EMA_ERR_INVAL, "sched_place: bad arguments");
-  auto& mine = s->placed[{gpu, req}];
+  // allocate first: a failed host allocation changes nothing
+  auto slot = s->placed.try_emplace({gpu, req}).first;
+  auto& mine = slot->second;
+  try {
+    mine.reserve(mine.size() + size_t(n));
+  } catch (...) {
+    if (mine.empty()) s->placed.erase(slot);
+    throw;
+  }
   int32_t done = 0;
   for (int32_t k = 0; k < n; ++k) {
     int32_t best = -1;
@@ -75,9 +88,11 @@ int ema_sched_place(ema_sched_t s, int32_t gpu, int32_t req, int32_t n, int64_t 
   }
   if (placed) *placed = done;
   return EMA_OK;
+} catch (...) {
+  return ema::internal_error();
 }
 
-int ema_sched_release(ema_sched_t s, int32_t gpu, int32_t req, int32_t n) {
+int ema_sched_release(ema_sched_t s, int32_t gpu, int32_t req, int32_t n) try {
   if (!s || gpu < 0 || gpu >= s->m || n < 0)
     return set_error(EMA_ERR_INVAL, "sched_release: bad arguments");
   auto it = s->placed.find({gpu, req});
@@ -89,9 +104,11 @@ int ema_sched_release(ema_sched_t s, int32_t gpu, int32_t req, int32_t n) {
   }
   if (it != s->placed.end() && it->second.empty()) s->placed.erase(it);
   return EMA_OK;
+} catch (...) {
+  return ema::internal_error();
 }
 
-int ema_sched_preempted(ema_sched_t s, int32_t gpu, int32_t peer, int64_t t) {
+int ema_sched_preempted(ema_sched_t s, int32_t gpu, int32_t peer, int64_t t) try {
   if (!s || gpu < 0 || gpu >= s->m || peer < 0 || peer >= s->m || peer == gpu)
     return set_error(EMA_ERR_INVAL, "sched_preempted: bad arguments");
   if (s->window == 0) return EMA_OK;
@@ -102,15 +119,19 @@ int ema_sched_preempted(ema_sched_t s, int32_t gpu, int32_t peer, int64_t t) {
   if (!s->capped(gpu, peer, t) || level < s->cap[e]) s->cap[e] = level;
   s->cap_until[e] = t + s->window;
   return EMA_OK;
+} catch (...) {
+  return ema::internal_error();
 }
 
-int ema_sched_usage(ema_sched_t s, int64_t t, int32_t* use, int32_t* cap) {
+int ema_sched_usage(ema_sched_t s, int64_t t, int32_t* use, int32_t* cap) try {
   if (!s || !use) return set_error(EMA_ERR_INVAL, "sched_usage: NULL argument");
   for (size_t e = 0; e < s->use.size(); ++e) {
     use[e] = s->use[e];
     if (cap) cap[e] = s->capped(int32_t(e / s->m), int32_t(e % s->m), t) ? s->cap[e] : -1;
   }
   return EMA_OK;
+} catch (...) {
+  return ema::internal_error();
 }
 
 }  // extern "C"

@@ -133,3 +133,38 @@ def test_large_pool_reclaim_plan_matches_oracle():
         oracle.check_ownership(st, cache.tables)
     finally:
         lib.close()
+
+
+def test_library_reclaim_victim_order_hand_worked():
+    """Step 4 of reclaim on the library: owners ranked by movers in the
+    returned range, ties to the larger id, preempted until the rest fit."""
+    lib = LibHostBackend(3, 6)
+    ema = lib.ema
+    try:
+        lib.alloc_blocks(ema.POOL_LOCAL, [7, 7, 7])
+        lib.free_blocks([0, 1])                                    # local 0, 1 free
+        lib.alloc_blocks(ema.POOL_SLICE, [5, 6, 2, 2, 3, 3])       # slots 0..5
+        r = lib.reclaim(4, np.full((1, 1), -1))                    # range: slots 2..5
+        # owners 2 and 3 hold two movers each, two destinations (local 0, 1):
+        # the larger id is preempted, owner 2's blocks are written back
+        assert r["victims"] == [3] and r["moved"] == 2 and r["written_back"] == 2
+        assert np.asarray(r["moves"]).tolist() == [[5, 0], [6, 1]]
+        own_l, own_s, lim = lib.owners()
+        assert own_l.tolist() == [2, 2, 7] and lim == 2
+        assert own_s.tolist()[:2] == [5, 6]
+    finally:
+        lib.close()
+    lib = LibHostBackend(1, 8)
+    ema = lib.ema
+    try:
+        lib.alloc_blocks(ema.POOL_LOCAL, [4])
+        lib.alloc_blocks(ema.POOL_SLICE, [1, 4, 9, 9, 4, 1, 1, 1])  # slots 0..7
+        r = lib.reclaim(6, np.full((1, 1), -1))                    # range: slots 2..7
+        # movers: owner 1 x3, 9 x2, 4 x1; no destinations. Owner 1 goes
+        # first (which frees slot 0), then 9; owner 4's mover at slot 4 takes
+        # slot 0, and owner 4 keeps its local block
+        assert r["victims"] == [1, 9] and r["moves"].tolist() == [[5, 1]]
+        own_l, own_s, lim = lib.owners()
+        assert own_l.tolist() == [4] and own_s.tolist()[:2] == [4, 4]
+    finally:
+        lib.close()
