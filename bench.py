@@ -4,12 +4,17 @@
 One step = one decode iteration over every layer of a synthetic paged KV cache
 (Llama-3-8B-shaped by default: 32 layers, 32/8 heads, head dim 128, bf16,
 block 16, batch 64, lengths U[1024, 4096], 30 % of each layer's blocks in the
-slice). Per layer: the slice-resident blocks of layer l+1 are prefetched into a
-double-buffered staging area on one stream while paged decode attention of
-layer l runs on another (``--mode serial`` runs both on one stream: copy, then
-attention, the on-demand swap of the paper's ablation; ``--append`` also stores
-a new token per sequence before each layer's attention and writes the modified
-staged blocks back to the slice after it).
+slice). Per layer, the slice-resident blocks are prefetched into a staging
+area and paged decode attention reads them from there. Two schedules:
+``--mode serial`` (the default) runs each layer's prefetch and attention on one
+stream; ``--mode overlap`` prefetches layer l+1 on a second stream while
+attention of layer l runs, with ``--slots`` staging slots. On one GPU the slice
+shares the HBM with attention, so both schedules are bound by the same bytes;
+the other schedule's steps are timed after the headline ones and reported as
+``alt_mode``. ``--append`` also stores a new token per sequence before each
+layer's attention and writes the modified staged blocks back to the slice
+after it. Each step times a few layers' calls with events (rotating), since
+every event costs device time.
 
 After the timed steps, untimed by the step clock:
   * symmetry: attention over every layer through the staged tables versus
@@ -58,7 +63,15 @@ def parse():
     ap.add_argument("--workload", default="llama3-8b-kv",
                     choices=["llama3-8b-kv", "llama-70b-tp8-share", "bursty-8b", "stress",
                              "slab-sweep"])
-    ap.add_argument("--mode", default="overlap", choices=["overlap", "serial"])
+    ap.add_argument("--mode", default="serial", choices=["serial", "overlap"],
+                    help="serial: prefetch then attention on one stream; overlap: prefetch of "
+                         "layer l+1 on a second stream during attention of layer l")
+    ap.add_argument("--no-alt-mode", action="store_true",
+                    help="skip the steps in the other mode that are reported alongside")
+    ap.add_argument("--slots", type=int, default=2,
+                    help="staging slots; the copy stream prefetches up to slots-1 layers ahead")
+    ap.add_argument("--timed-layers", type=int, default=2,
+                    help="layers per step whose calls get timing events (rotating)")
     ap.add_argument("--append", action="store_true",
                     help="each layer also appends the new token's K/V and writes the modified "
                          "staged blocks back to the slice")
@@ -211,6 +224,31 @@ def symmetry(w, out, s, reps, ema, torch):
             "reps": reps, "moved_blocks": int(len(src))}
 
 
+def alt_mode_steps(w, out, mode, args, attn_b):
+    """The same steps in the other schedule, timed the same way (reported beside
+    the headline, not part of it)."""
+    import torch
+    from harness import StepRunner
+    log(f"{mode} steps for comparison")
+    runner = StepRunner(w, mode)
+    for _ in range(args.warmup):
+        runner.run(out)
+    L = w.L
+    nt = max(1, min(L, args.timed_layers))
+    timers = [runner.new_timers([(nt * k + i) % L for i in range(nt)])
+              for k in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        runner.run(out, timers[k])
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    at_us = float(np.mean([e0.elapsed_time(e1) for tm in timers
+                           for e0, e1 in tm["at"].values()])) * 1e3
+    return {"mode": mode, "ms_per_step": ms_step, "tokens_per_s": w.B / (ms_step / 1e3),
+            "attention_mean_us": at_us, "attention_GBps": attn_b / at_us / 1e3}
+
+
 def reclaim_phase(w, s, reps, ema, torch):
     """The lender takes 5 % of its lent blocks back, ``reps`` times. Each call is
     queued behind a device copy long enough to outlast the call's host planning,
@@ -246,7 +284,7 @@ def bursty_main(args):
     torch.cuda.set_device(0)
     cfg = synth.BURSTY
     log("setting up bursty-8b")
-    tr = BurstyTrace(cfg, fill="device")
+    tr = BurstyTrace(cfg, fill="device", mode=args.mode)
     w = tr.w
     steps = cfg.extra["steps"]
     recs, gbps = [], []
@@ -277,7 +315,8 @@ def bursty_main(args):
         "config": {"workload": cfg.name, "layers": w.L, "batch": w.B, "q_heads": cfg.q_heads,
                    "kv_heads": cfg.kv_heads, "head_dim": cfg.head_dim,
                    "block_size": cfg.block_size, "lens": list(cfg.lens),
-                   "frac_max": cfg.extra["frac_max"], "step_frac": list(cfg.extra["step_frac"])},
+                   "frac_max": cfg.extra["frac_max"], "step_frac": list(cfg.extra["step_frac"]),
+                   "mode": args.mode},
         "step_ms": {"p10": pct(ms, 10), "p50": pct(ms, 50), "p90": pct(ms, 90),
                     "max": float(ms.max())},
         "step_GBps": {"p10": pct(gbps, 10), "p50": pct(gbps, 50), "p90": pct(gbps, 90)},
@@ -392,7 +431,7 @@ def main():
                             np.random.default_rng(cfg.seed))
     extra = len(probe.slice_order) if args.symmetry_reps > 0 else 0
     del probe
-    w = Workload(cfg, fill="device", extra_local=extra)
+    w = Workload(cfg, fill="device", extra_local=extra, staging_slots=max(2, args.slots))
     L, B = w.L, w.B
     log(f"{L} layers, batch {B}, {w.n_local} local + {w.slice_view.shape[0]} slice blocks")
     runner = StepRunner(w, args.mode, append=args.append)
@@ -405,7 +444,11 @@ def main():
     for _ in range(args.warmup):
         runner.run(out)
     torch.cuda.synchronize()
-    timers = [runner.new_timers() for _ in range(args.steps)]
+    # every timing event costs device time, so each step times a few layers
+    # (rotating over the steps) and the rest run without events
+    nt = max(1, min(L, args.timed_layers))
+    timers = [runner.new_timers([(nt * k + i) % L for i in range(nt)])
+              for k in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -417,15 +460,19 @@ def main():
     if errs:
         raise RuntimeError(f"kernels skipped {errs} invalid ids")
 
-    at_ms = np.array([[tm["at"][l][0].elapsed_time(tm["at"][l][1]) for l in range(L)]
-                      for tm in timers])
-    pf_ms = np.array([[tm["pf"][l][0].elapsed_time(tm["pf"][l][1]) for l in range(L)]
-                      for tm in timers])
+    at_ms = np.array([e0.elapsed_time(e1) for tm in timers for e0, e1 in tm["at"].values()])
+    pf_ms = np.array([e0.elapsed_time(e1) for tm in timers for e0, e1 in tm["pf"].values()])
+    pf_timed_b = float(sum(pf_b[l] for tm in timers for l in tm["pf"]))
     at_mean_s = float(at_ms.mean()) / 1e3
     attn_gbps = attn_b / at_mean_s / 1e9
-    pf_gbps = float(np.sum(pf_b) * args.steps / (pf_ms.sum() / 1e3) / 1e9)
+    pf_gbps = pf_timed_b / (pf_ms.sum() / 1e3) / 1e9
     step_bytes = attn_b * L + float(np.sum(pf_b))
     log(f"{ms_step:.3f} ms/step, attention {at_mean_s * 1e6:.1f} us/layer")
+
+    alt = None
+    if not args.no_alt_mode:
+        alt = alt_mode_steps(w, out, "overlap" if args.mode == "serial" else "serial",
+                             args, attn_b)
 
     traffic = None
     rec = counter_traffic(cfg.name)
@@ -448,11 +495,13 @@ def main():
         "config": {"workload": cfg.name, "layers": L, "batch": B, "q_heads": cfg.q_heads,
                    "kv_heads": cfg.kv_heads, "head_dim": cfg.head_dim,
                    "block_size": cfg.block_size, "lens": list(cfg.lens),
-                   "slice_frac": cfg.slice_frac, "mode": args.mode, "append": args.append},
+                   "slice_frac": cfg.slice_frac, "mode": args.mode, "append": args.append,
+                   "staging_slots": w.staging_slots},
         "roofline": {"bound": "hbm", "achieved": attn_gbps, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": attn_gbps / HBM_PEAK_GBPS, "traffic": traffic,
                      "kernel": "paged_decode_attention (attn_mfma_streamk + attn_combine_streamk)"},
-        "attention": {"bytes_per_launch": attn_b, "mean_us": at_mean_s * 1e6,
+        "attention": {"bytes_per_launch": attn_b, "timed_calls": int(at_ms.size),
+                      "mean_us": at_mean_s * 1e6,
                       "p10_us": pct(at_ms, 10) * 1e3, "p90_us": pct(at_ms, 90) * 1e3,
                       "GBps": attn_gbps, "frac": attn_gbps / HBM_PEAK_GBPS},
         "prefetch": {"bytes_per_step": float(np.sum(pf_b)), "mean_us": float(pf_ms.mean()) * 1e3,
@@ -462,6 +511,8 @@ def main():
     }
     if rec is not None:
         res["roofline"]["traffic_source"] = rec.get("note", "counter summary")
+    if alt is not None:
+        res["alt_mode"] = alt
 
     if args.symmetry_reps > 0:
         log("symmetry: staged vs all-local tables")

@@ -49,6 +49,11 @@ constexpr int kPieceTiles = 32;            // tiles whose block ids are staged i
 constexpr int kMaxIds = kPieceTiles * kIt / 16;
 constexpr int kMaxPersistBatch = 2048;     // sequences the stream-K work list holds in LDS
 constexpr int kGridChunkTiles = 32;        // tiles per workgroup in the grid fallback
+// Starting a (sequence, KV head) costs a workgroup about five tiles' time (its
+// pipeline drains and refills, the four wavefronts merge, a partial is
+// written), measured on 32-token tiles; the stream-K split counts it so that
+// workgroups that touch more pairs get fewer tiles.
+constexpr int kSegCost = 5;
 
 __device__ __forceinline__ u32x4 ld16(const char* p) {
   return *reinterpret_cast<const u32x4*>(p);
@@ -308,8 +313,9 @@ __device__ __forceinline__ void write_zeros(const AttnArgs& a, int b) {
 }
 
 // Stream-K form. Every workgroup reads all lengths once and prefix-sums the
-// tile counts n_t(b) * Hkv in LDS; units are ordered (sequence, KV head,
-// tile) and workgroup w takes units [w*per, (w+1)*per), per = ceil(U/grid).
+// unit counts (n_t(b) + kSegCost) * Hkv in LDS; units are ordered (sequence,
+// KV head, unit), each pair's kSegCost cost units (no tiles) ahead of its n_t
+// tiles, and workgroup w takes units [w*per, (w+1)*per), per = ceil(U/grid).
 // For each (sequence, KV head) it touches, it writes the output directly when
 // it holds all of that pair's tiles, else a partial into slot 2w (its first
 // pair) or 2w+1 (its last pair). The workgroup that holds a pair's first tile
@@ -334,7 +340,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_streamk(AttnArgs a) {
     if (blockIdx.x == 0 && len != raw && raw > 0) atomicAdd(a.err_count, 1);
     s_len[b] = len;
     s_pref[b] = run;
-    run += (len + kIt - 1) / kIt * H;
+    const int nt_b = (len + kIt - 1) / kIt;
+    run += nt_b > 0 ? (nt_b + kSegCost) * H : 0;
   }
   s_seg[tid] = run;
   __syncthreads();
@@ -370,7 +377,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_streamk(AttnArgs a) {
   const int per = (U + int(gridDim.x) - 1) / int(gridDim.x);
   int u = min(U, int(blockIdx.x) * per);
   const int u_end = min(U, u + per);
-  for (int seg = 0; u < u_end; ++seg) {
+  int seg = 0;
+  while (u < u_end) {
     int lo = 0, hi = B - 1;   // last sequence whose first unit is <= u
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
@@ -380,9 +388,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_streamk(AttnArgs a) {
     const int b = uniform(lo);
     const int len = uniform(s_len[b]);
     const int nt = (len + kIt - 1) / kIt;
+    const int P = nt + kSegCost;            // a pair's units: kSegCost, then its tiles
     const int r = u - uniform(s_pref[b]);
-    const int kvh = r / nt;
-    const int j0 = r - kvh * nt;
+    const int kvh = r / P;
+    const int q = r - kvh * P;
+    if (q < kSegCost) {                      // cost units carry no tiles
+      u += kSegCost - q;
+      continue;
+    }
+    const int j0 = q - kSegCost;
     const int j1 = min(nt, j0 + (u_end - u));
     const bool whole = j0 == 0 && j1 == nt;
     const int64_t slot = int64_t(blockIdx.x) * 2 + (seg == 0 ? 0 : 1);
@@ -401,10 +415,11 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_streamk(AttnArgs a) {
     if (j0 == 0 && tid == 0) {
       int32_t* info = a.info + (int64_t(b) * H + kvh) * 3;
       info[0] = int(blockIdx.x);
-      info[1] = (uniform(s_pref[b]) + kvh * nt + nt - 1) / per;
+      info[1] = (uniform(s_pref[b]) + kvh * P + P - 1) / per;
       info[2] = seg == 0 ? 0 : 1;
     }
     u += j1 - j0;
+    ++seg;
   }
 }
 

@@ -3,6 +3,7 @@
 
 #include <algorithm>
 #include <functional>
+#include <unordered_map>
 #include <unordered_set>
 
 namespace ema {
@@ -251,14 +252,19 @@ int SliceBook::reclaim(int32_t n, ReclaimPlan* p, std::string* err) {
   for (int32_t s = cut; s < lim_; ++s)
     if (own_slice_[s] >= 0) movers.push_back(s);
   const size_t m0 = movers.size();
+  auto n_dest = [&]() {
+    return int64_t(free_slice_.count_below(cut)) + free_local_.count();
+  };
   // Preempting an owner removes only its own movers, so the owners ranked
-  // once by (movers desc, id desc) give the order in which step 4 takes them.
-  std::vector<std::pair<int32_t, int32_t>> rank;   // (count, owner)
-  {
+  // once by (movers desc, id desc) give the order in which step 4 takes them,
+  // and each preemption adds the owner's local blocks and its slice blocks
+  // below the cut to the destinations: the victims follow from counts alone.
+  std::vector<std::vector<int32_t>> held;      // blocks of each victim, ascending
+  if (int64_t(m0) > n_dest()) {
     std::vector<int32_t> own(m0);
     for (size_t i = 0; i < m0; ++i) own[i] = own_slice_[movers[i]];
     std::sort(own.begin(), own.end());
-    rank.reserve(m0);
+    std::vector<std::pair<int32_t, int32_t>> rank;   // (movers, owner)
     for (size_t i = 0; i < m0;) {
       size_t j = i;
       while (j < m0 && own[j] == own[i]) ++j;
@@ -266,32 +272,47 @@ int SliceBook::reclaim(int32_t n, ReclaimPlan* p, std::string* err) {
       i = j;
     }
     std::sort(rank.begin(), rank.end(), std::greater<std::pair<int32_t, int32_t>>());
+    std::unordered_map<int32_t, size_t> pos;         // owner -> rank position
+    pos.reserve(rank.size() * 2);
+    for (size_t k = 0; k < rank.size(); ++k) pos[rank[k].second] = k;
+    std::vector<int64_t> frees(rank.size(), 0);      // destinations its preemption adds
+    for (int32_t u = 0; u < n_local_; ++u) {
+      auto it = own_local_[u] >= 0 ? pos.find(own_local_[u]) : pos.end();
+      if (it != pos.end()) ++frees[it->second];
+    }
+    for (int32_t s = 0; s < cut; ++s) {
+      auto it = own_slice_[s] >= 0 ? pos.find(own_slice_[s]) : pos.end();
+      if (it != pos.end()) ++frees[it->second];
+    }
+    int64_t alive = int64_t(m0), dest = n_dest();
+    size_t nv = 0;
+    while (alive > dest) {
+      alive -= rank[nv].first;
+      dest += frees[nv];
+      ++nv;
+    }
+    held.resize(nv);
+    for (int32_t u = 0; u < n_local_ + n_slice_; ++u) {
+      const int32_t o = u < n_local_ ? own_local_[u] : own_slice_[u - n_local_];
+      auto it = o >= 0 ? pos.find(o) : pos.end();
+      if (it != pos.end() && it->second < nv) held[it->second].push_back(u);
+    }
+    p->victims.reserve(nv);
+    size_t total = 0;
+    for (const auto& v : held) total += v.size();
+    p->victim_blocks.reserve(total);
+    for (size_t k = 0; k < nv; ++k) p->victims.push_back(rank[k].second);
   }
   std::vector<int32_t> dst(m0);
-  p->victims.reserve(rank.size());
-  p->victim_blocks.reserve(size_t(n_local_) + size_t(n_slice_));
   p->move_src.reserve(m0);
   p->move_dst.reserve(m0);
 
-  auto n_dest = [&]() {
-    return int64_t(free_slice_.count_below(cut)) + free_local_.count();
-  };
-  int64_t alive = int64_t(m0);
-  for (size_t k = 0; alive > n_dest(); ++k) {
-    const int32_t best = rank[k].second;
-    alive -= rank[k].first;
-    p->victims.push_back(best);
-    for (int32_t u = 0; u < n_local_; ++u)
-      if (own_local_[u] == best) {
-        p->victim_blocks.push_back(u);
-        set_owner(u, kFree);
-      }
-    for (int32_t s = 0; s < n_slice_; ++s)
-      if (own_slice_[s] == best) {
-        p->victim_blocks.push_back(n_local_ + s);
-        set_owner(n_local_ + s, kFree);
-      }
-  }
+  // ---- from here on the book changes and nothing allocates ----
+  for (const auto& blocks : held)
+    for (int32_t u : blocks) {
+      p->victim_blocks.push_back(u);
+      set_owner(u, kFree);
+    }
   if (!p->victims.empty())
     movers.erase(std::remove_if(movers.begin(), movers.end(),
                                 [&](int32_t s) { return own_slice_[s] < 0; }),
@@ -301,7 +322,7 @@ int SliceBook::reclaim(int32_t n, ReclaimPlan* p, std::string* err) {
   const int32_t got_s = free_slice_.lowest(m, cut, dst.data());
   for (int32_t i = 0; i < got_s; ++i) dst[i] += n_local_;
   const int32_t got_l = free_local_.lowest(m - got_s, n_local_, dst.data() + got_s);
-  // got_s + got_l == m: the loop above stops only once m <= n_dest()
+  // got_s + got_l == m: the victims were chosen so that m <= n_dest()
   for (int32_t i = 0; i < m; ++i) {
     const int32_t o = own_slice_[movers[i]];
     p->move_src.push_back(n_local_ + movers[i]);

@@ -40,7 +40,7 @@ def _round_half_up(x):
 class BurstyTrace:
     def __init__(self, cfg, layers=None, batch=None, seed=None, fill="device", mirror=None,
                  fmax=None, slack=0.02, f0=None, lens=None, slice_layout=ema.LAYOUT_ATTN,
-                 local_frac=1.0):
+                 local_frac=1.0, mode="serial"):
         cfg = cfg if batch is None else cfg.scaled(batch=batch)
         fmax = cfg.extra.get("frac_max", 0.7) if fmax is None else fmax
         L = cfg.layers if layers is None else layers
@@ -65,7 +65,7 @@ class BurstyTrace:
         self.f = f0
         self.step_no = 0
         self.log = []
-        self.runner = StepRunner(w, "overlap")
+        self.runner = StepRunner(w, mode)
         self.out = w.new_out()
         self.fill = fill
         self.readmitted = set()

@@ -230,58 +230,65 @@ class Workload:
 
 
 class StepRunner:
-    """One decode step of a workload: for every layer, prefetch of layer l+1 on
-    the copy stream while attention of layer l runs on the attention stream
-    (``mode="serial"``: one stream, copy then attention). Staging slot l % 2 is
-    refilled only after the attention that last read it; attention of layer l
-    waits for its own prefetch. With ``append``, each layer first stores the
-    new token's K/V (into the staged copy where the block is in the slice) and
-    the modified staged copies are written back on the copy stream after the
-    layer's attention, before the slot is refilled. ``timers`` (optional)
-    receives per-layer event pairs: {"pf": [(start, end)] * L, "at": [...]}."""
+    """One decode step of a workload. With S = ``w.staging_slots`` staging
+    slots, the copy stream prefetches up to S - 1 layers ahead of the attention
+    stream: layer l's slice blocks go to slot l % S, which is refilled only
+    after the attention that last read it; attention of layer l waits for its
+    own prefetch (``mode="serial"``: one stream, copy then attention). With
+    ``append``, each layer first stores the new token's K/V (into the staged
+    copy where the block is in the slice) and the modified staged copies are
+    written back on the copy stream after the layer's attention, before the
+    slot is refilled. ``timers`` (optional) maps a layer to the event pairs
+    recorded around its calls: {"pf": {l: (start, end)}, "at": {l: (...)}};
+    layers missing from a map are not timed (every timing event costs device
+    time)."""
 
     def __init__(self, w, mode="overlap", append=False):
         self.w = w
         self.kv_new = w.new_token_kv() if append else None
         self.s1 = torch.cuda.Stream()
         self.s2 = torch.cuda.Stream() if mode == "overlap" else self.s1
+        self.ahead = max(1, w.staging_slots - 1)
         self.ev_pf = [torch.cuda.Event() for _ in range(w.L)]
         self.ev_at = [torch.cuda.Event() for _ in range(w.L)]
 
-    def new_timers(self):
+    def new_timers(self, layers=None):
         mk = lambda: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-        return {"pf": [mk() for _ in range(self.w.L)], "at": [mk() for _ in range(self.w.L)]}
+        layers = range(self.w.L) if layers is None else layers
+        return {"pf": {l: mk() for l in layers}, "at": {l: mk() for l in layers}}
 
     def _prefetch(self, l, timers):
-        if timers:
-            timers["pf"][l][0].record(self.s2)
+        t = timers["pf"].get(l) if timers else None
+        if t:
+            t[0].record(self.s2)
         self.w.prefetch(l, stream=self.s2)
-        if timers:
-            timers["pf"][l][1].record(self.s2)
+        if t:
+            t[1].record(self.s2)
         self.ev_pf[l].record(self.s2)
 
     def run(self, out, timers=None):
         w, s1, s2 = self.w, self.s1, self.s2
-        L = w.L
+        L, S, ahead = w.L, w.staging_slots, self.ahead
         for l in range(L):
             if l == 0:
-                # staging slots 0/1 were last read by the previous step's last layers
+                # every slot was last read by the previous step's attention
                 s2.wait_event(self.ev_at[L - 1])
-                if L >= 2:
-                    s2.wait_event(self.ev_at[L - 2])
-                self._prefetch(0, timers)
-            if l + 1 < L:
-                if l >= 1:
-                    s2.wait_event(self.ev_at[l - 1])   # slot (l+1) % 2 was read by layer l-1
-                self._prefetch(l + 1, timers)
+                for k in range(min(ahead, L)):
+                    self._prefetch(k, timers)
+            k = l + ahead
+            if k < L:
+                if k - S >= 0:
+                    s2.wait_event(self.ev_at[k - S])   # slot k % S was read by layer k - S
+                self._prefetch(k, timers)
             s1.wait_event(self.ev_pf[l])
             if self.kv_new is not None:
                 w.append(l, *self.kv_new, stream=s1)
-            if timers:
-                timers["at"][l][0].record(s1)
+            t = timers["at"].get(l) if timers else None
+            if t:
+                t[0].record(s1)
             w.attention(l, out, stream=s1)
-            if timers:
-                timers["at"][l][1].record(s1)
+            if t:
+                t[1].record(s1)
             self.ev_at[l].record(s1)
             if self.kv_new is not None:
                 s2.wait_event(self.ev_at[l])
