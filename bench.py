@@ -68,8 +68,10 @@ def parse():
                          "layer l+1 on a second stream during attention of layer l")
     ap.add_argument("--no-alt-mode", action="store_true",
                     help="skip the steps in the other mode that are reported alongside")
-    ap.add_argument("--slots", type=int, default=2,
-                    help="staging slots; the copy stream prefetches up to slots-1 layers ahead")
+    ap.add_argument("--group", type=int, default=4,
+                    help="layers per layer group: one prefetch call per group")
+    ap.add_argument("--slots", type=int, default=None,
+                    help="staging slots, a multiple of the group size (default: two groups)")
     ap.add_argument("--timed-layers", type=int, default=2,
                     help="layers per step whose calls get timing events (rotating)")
     ap.add_argument("--append", action="store_true",
@@ -284,7 +286,7 @@ def bursty_main(args):
     torch.cuda.set_device(0)
     cfg = synth.BURSTY
     log("setting up bursty-8b")
-    tr = BurstyTrace(cfg, fill="device", mode=args.mode)
+    tr = BurstyTrace(cfg, fill="device", mode=args.mode, group=args.group)
     w = tr.w
     steps = cfg.extra["steps"]
     recs, gbps = [], []
@@ -316,7 +318,7 @@ def bursty_main(args):
                    "kv_heads": cfg.kv_heads, "head_dim": cfg.head_dim,
                    "block_size": cfg.block_size, "lens": list(cfg.lens),
                    "frac_max": cfg.extra["frac_max"], "step_frac": list(cfg.extra["step_frac"]),
-                   "mode": args.mode},
+                   "mode": args.mode, "layer_group": args.group},
         "step_ms": {"p10": pct(ms, 10), "p50": pct(ms, 50), "p90": pct(ms, 90),
                     "max": float(ms.max())},
         "step_GBps": {"p10": pct(gbps, 10), "p50": pct(gbps, 50), "p90": pct(gbps, 90)},
@@ -431,14 +433,16 @@ def main():
                             np.random.default_rng(cfg.seed))
     extra = len(probe.slice_order) if args.symmetry_reps > 0 else 0
     del probe
-    w = Workload(cfg, fill="device", extra_local=extra, staging_slots=max(2, args.slots))
+    g = max(1, args.group)
+    slots = 2 * g if args.slots is None else args.slots
+    w = Workload(cfg, fill="device", extra_local=extra, staging_slots=slots, group=g)
     L, B = w.L, w.B
     log(f"{L} layers, batch {B}, {w.n_local} local + {w.slice_view.shape[0]} slice blocks")
     runner = StepRunner(w, args.mode, append=args.append)
     s1 = runner.s1
     out = w.new_out()
     attn_b = attention_bytes(w)
-    pf_b = [2 * len(w.pf_src[l]) * w.bb for l in range(L)]
+    pf_b = [2 * len(src) * w.bb for src in w.pf_src_grp]      # per layer group
 
     log(f"warmup {args.warmup}, timed {args.steps} steps ({args.mode})")
     for _ in range(args.warmup):
@@ -462,7 +466,7 @@ def main():
 
     at_ms = np.array([e0.elapsed_time(e1) for tm in timers for e0, e1 in tm["at"].values()])
     pf_ms = np.array([e0.elapsed_time(e1) for tm in timers for e0, e1 in tm["pf"].values()])
-    pf_timed_b = float(sum(pf_b[l] for tm in timers for l in tm["pf"]))
+    pf_timed_b = float(sum(pf_b[k] for tm in timers for k in tm["pf"]))
     at_mean_s = float(at_ms.mean()) / 1e3
     attn_gbps = attn_b / at_mean_s / 1e9
     pf_gbps = pf_timed_b / (pf_ms.sum() / 1e3) / 1e9
@@ -496,7 +500,7 @@ def main():
                    "kv_heads": cfg.kv_heads, "head_dim": cfg.head_dim,
                    "block_size": cfg.block_size, "lens": list(cfg.lens),
                    "slice_frac": cfg.slice_frac, "mode": args.mode, "append": args.append,
-                   "staging_slots": w.staging_slots},
+                   "layer_group": w.group, "staging_slots": w.staging_slots},
         "roofline": {"bound": "hbm", "achieved": attn_gbps, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": attn_gbps / HBM_PEAK_GBPS, "traffic": traffic,
                      "kernel": "paged_decode_attention (attn_mfma_streamk + attn_combine_streamk)"},

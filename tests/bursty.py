@@ -40,7 +40,7 @@ def _round_half_up(x):
 class BurstyTrace:
     def __init__(self, cfg, layers=None, batch=None, seed=None, fill="device", mirror=None,
                  fmax=None, slack=0.02, f0=None, lens=None, slice_layout=ema.LAYOUT_ATTN,
-                 local_frac=1.0, mode="serial"):
+                 local_frac=1.0, mode="serial", group=1):
         cfg = cfg if batch is None else cfg.scaled(batch=batch)
         fmax = cfg.extra.get("frac_max", 0.7) if fmax is None else fmax
         L = cfg.layers if layers is None else layers
@@ -58,7 +58,8 @@ class BurstyTrace:
         self.w = w = Workload(cfg, layers=L, seed=seed, fill=fill, frac=f0, lens=lens,
                               stage_n=n_l, extra_local=n_local - (T - slice0),
                               extra_slice=n_slice - slice0,
-                              slice_layout=slice_layout)
+                              slice_layout=slice_layout, group=group,
+                              staging_slots=2 * group)
         self.cfg, self.L, self.B, self.T, self.fmax = cfg, L, w.B, T, fmax
         self.n_slice = n_slice
         self.rng = np.random.default_rng(seed + 1000)

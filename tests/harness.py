@@ -25,7 +25,7 @@ TORCH_DT = {"f16": torch.float16, "bf16": torch.bfloat16}
 class Workload:
     def __init__(self, cfg, layers=None, batch=None, slice_layout=ema.LAYOUT_ATTN, seed=None,
                  staging_slots=2, extra_local=0, extra_slice=0, fill="host", checked=False,
-                 lens=None, frac=None, shuffle=True, stage_n=None):
+                 lens=None, frac=None, shuffle=True, stage_n=None, group=1):
         self.cfg = cfg = cfg if batch is None else cfg.scaled(batch=batch)
         self.L = cfg.layers if layers is None else layers
         rng = np.random.default_rng(cfg.seed if seed is None else seed)
@@ -41,6 +41,7 @@ class Workload:
         self.stage_n = (int(self.slice_per_layer.max()) if self.L else 0) if stage_n is None \
             else int(stage_n)
         self.staging_slots = staging_slots
+        self.group = max(1, int(group))
         n_local = len(pl.local_order) + staging_slots * self.stage_n + extra_local
         n_slice = len(pl.slice_order) + extra_slice
         self.h = ema.slice_create(self.hkv, self.D, self.bs, cfg.dtype, slice_layout,
@@ -164,6 +165,20 @@ class Workload:
             self.attn_dev.copy_(a32)
         self.pf_src_dev = [torch.from_numpy(s).to(dev) for s in self.pf_src]
         self.pf_dst_dev = [torch.from_numpy(d).to(dev) for d in self.pf_dst]
+        # one list per layer group (consecutive layers, swapped together)
+        g = self.group
+        self.groups = [list(range(k, min(self.L, k + g))) for k in range(0, self.L, g)]
+        self.pf_src_grp, self.pf_dst_grp = [], []
+        for ls in self.groups:
+            src = np.concatenate([self.pf_src[l] for l in ls]) if ls else np.zeros(0, np.int32)
+            dst = np.concatenate([self.pf_dst[l] for l in ls]) if ls else np.zeros(0, np.int32)
+            self.pf_src_grp.append(src)
+            self.pf_dst_grp.append(dst)
+        if g == 1:
+            self.pf_src_grp_dev, self.pf_dst_grp_dev = self.pf_src_dev, self.pf_dst_dev
+        else:
+            self.pf_src_grp_dev = [torch.from_numpy(s).to(dev) for s in self.pf_src_grp]
+            self.pf_dst_grp_dev = [torch.from_numpy(d).to(dev) for d in self.pf_dst_grp]
         self.wb_src_dev = [torch.from_numpy(s).to(dev) for s in self.wb_src]
         self.wb_dst_dev = [torch.from_numpy(d).to(dev) for d in self.wb_dst]
 
@@ -184,6 +199,11 @@ class Workload:
     def prefetch(self, l, stream=None):
         ema.slice_prefetch(self.h, self.pf_src_dev[l], self.pf_dst_dev[l], len(self.pf_src[l]),
                            stream=stream)
+
+    def prefetch_group(self, k, stream=None):
+        """Every slice-resident block of layer group k in one call."""
+        ema.slice_prefetch(self.h, self.pf_src_grp_dev[k], self.pf_dst_grp_dev[k],
+                           len(self.pf_src_grp[k]), stream=stream)
 
     def append(self, l, k_new, v_new, stream=None):
         ema.kv_append(self.h, k_new, v_new, self.attn_dev[l], self.lens_dev, stream=stream)
@@ -230,69 +250,85 @@ class Workload:
 
 
 class StepRunner:
-    """One decode step of a workload. With S = ``w.staging_slots`` staging
-    slots, the copy stream prefetches up to S - 1 layers ahead of the attention
-    stream: layer l's slice blocks go to slot l % S, which is refilled only
-    after the attention that last read it; attention of layer l waits for its
-    own prefetch (``mode="serial"``: one stream, copy then attention). With
-    ``append``, each layer first stores the new token's K/V (into the staged
-    copy where the block is in the slice) and the modified staged copies are
-    written back on the copy stream after the layer's attention, before the
-    slot is refilled. ``timers`` (optional) maps a layer to the event pairs
-    recorded around its calls: {"pf": {l: (start, end)}, "at": {l: (...)}};
-    layers missing from a map are not timed (every timing event costs device
-    time)."""
+    """One decode step of a workload, prefetching per layer group (the
+    workload's ``group`` consecutive layers, swapped together in one call).
+    Staging slot l % S holds layer l's staged blocks (S = ``w.staging_slots``,
+    a multiple of the group size), so S / group groups are in flight at most;
+    a group's slots are refilled only after the attention that last read them,
+    and attention of a layer waits for its group's prefetch.
+
+    ``mode="serial"``: one stream, each group's prefetch followed by its
+    layers' attention (with S = 2·group the next group's prefetch is queued
+    before the current group's attention, which is the same work in another
+    order). ``mode="overlap"``: prefetches on a second stream, up to
+    S / group − 1 groups ahead of the attention stream (needs S ≥ 2·group).
+
+    With ``append``, each layer first stores the new token's K/V (into the
+    staged copy where the block is in the slice) and the modified staged copies
+    are written back on the copy stream after the layer's attention, before
+    the slot is refilled. ``timers`` (optional) maps group index (``"pf"``) or
+    layer (``"at"``) to the event pair recorded around the call; entries
+    missing from a map are not timed (every timing event costs device time)."""
 
     def __init__(self, w, mode="overlap", append=False):
         self.w = w
+        g, S = w.group, w.staging_slots
+        if S % g or S < g or (mode == "overlap" and S < 2 * g):
+            raise ValueError(f"{S} staging slots do not fit groups of {g} layers ({mode})")
         self.kv_new = w.new_token_kv() if append else None
         self.s1 = torch.cuda.Stream()
         self.s2 = torch.cuda.Stream() if mode == "overlap" else self.s1
-        self.ahead = max(1, w.staging_slots - 1)
-        self.ev_pf = [torch.cuda.Event() for _ in range(w.L)]
+        self.unit_slots = S // g
+        self.ahead = self.unit_slots - 1
+        self.ev_pf = [torch.cuda.Event() for _ in range(len(w.groups))]
         self.ev_at = [torch.cuda.Event() for _ in range(w.L)]
 
-    def new_timers(self, layers=None):
+    def new_timers(self, layers=None, groups=None):
         mk = lambda: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
         layers = range(self.w.L) if layers is None else layers
-        return {"pf": {l: mk() for l in layers}, "at": {l: mk() for l in layers}}
+        if groups is None:
+            groups = sorted({l // self.w.group for l in layers})
+        return {"pf": {k: mk() for k in groups}, "at": {l: mk() for l in layers}}
 
-    def _prefetch(self, l, timers):
-        t = timers["pf"].get(l) if timers else None
+    def _prefetch(self, k, timers):
+        t = timers["pf"].get(k) if timers else None
         if t:
             t[0].record(self.s2)
-        self.w.prefetch(l, stream=self.s2)
+        self.w.prefetch_group(k, stream=self.s2)
         if t:
             t[1].record(self.s2)
-        self.ev_pf[l].record(self.s2)
+        self.ev_pf[k].record(self.s2)
 
     def run(self, out, timers=None):
         w, s1, s2 = self.w, self.s1, self.s2
-        L, S, ahead = w.L, w.staging_slots, self.ahead
-        for l in range(L):
-            if l == 0:
+        groups, US, ahead = w.groups, self.unit_slots, self.ahead
+        NG = len(groups)
+        for u in range(NG):
+            if u == 0:
                 # every slot was last read by the previous step's attention
-                s2.wait_event(self.ev_at[L - 1])
-                for k in range(min(ahead, L)):
+                s2.wait_event(self.ev_at[w.L - 1])
+                for k in range(min(ahead, NG)):
                     self._prefetch(k, timers)
-            k = l + ahead
-            if k < L:
-                if k - S >= 0:
-                    s2.wait_event(self.ev_at[k - S])   # slot k % S was read by layer k - S
+            k = u + ahead
+            if k < NG:
+                if k - US >= 0:
+                    # group k's slots were read by group k - US
+                    s2.wait_event(self.ev_at[groups[k - US][-1]])
                 self._prefetch(k, timers)
-            s1.wait_event(self.ev_pf[l])
-            if self.kv_new is not None:
-                w.append(l, *self.kv_new, stream=s1)
-            t = timers["at"].get(l) if timers else None
-            if t:
-                t[0].record(s1)
-            w.attention(l, out, stream=s1)
-            if t:
-                t[1].record(s1)
-            self.ev_at[l].record(s1)
-            if self.kv_new is not None:
-                s2.wait_event(self.ev_at[l])
-                w.writeback(l, stream=s2)
+            s1.wait_event(self.ev_pf[u])
+            for l in groups[u]:
+                if self.kv_new is not None:
+                    w.append(l, *self.kv_new, stream=s1)
+                t = timers["at"].get(l) if timers else None
+                if t:
+                    t[0].record(s1)
+                w.attention(l, out, stream=s1)
+                if t:
+                    t[1].record(s1)
+                self.ev_at[l].record(s1)
+                if self.kv_new is not None:
+                    s2.wait_event(self.ev_at[l])
+                    w.writeback(l, stream=s2)
 
 
 class BlockedTimer:

@@ -41,13 +41,16 @@ def _local_attention_reader(st):
                                           st.block_size)
 
 
-@pytest.mark.parametrize("layout,local_frac,mode", [(0, 1.0, "serial"), (0, 1.0, "overlap"),
-                                                    (1, 1.0, "overlap"), (1, 0.8, "serial")])
-def test_bursty_trace_scaled_matches_oracle(ema, layout, local_frac, mode):
+@pytest.mark.parametrize("layout,local_frac,mode,group", [(0, 1.0, "serial", 1),
+                                                          (0, 1.0, "overlap", 2),
+                                                          (1, 1.0, "overlap", 1),
+                                                          (1, 0.8, "serial", 2)])
+def test_bursty_trace_scaled_matches_oracle(ema, layout, local_frac, mode, group):
     from bursty import BurstyTrace
-    print(f"bursty scaled layout={layout} local_frac={local_frac} mode={mode}", flush=True)
+    print(f"bursty scaled layout={layout} local_frac={local_frac} mode={mode} group={group}",
+          flush=True)
     tr = BurstyTrace(synth.BURSTY, layers=4, batch=8, fill="host", mirror="data",
-                     slice_layout=layout, local_frac=local_frac, mode=mode)
+                     slice_layout=layout, local_frac=local_frac, mode=mode, group=group)
     try:
         st = tr.mirror
         logical0 = oracle.logical_view(st, tr.w.tables)

@@ -209,17 +209,19 @@ def test_decode_steps_with_append_and_writeback_match_oracle(ema, layout):
         w.close()
 
 
-@pytest.mark.parametrize("layout", [0, 1])
-def test_step_runner_append_reaches_every_block(ema, layout):
-    """The overlapped step with append: after one step every sequence's last
-    block, in every layer, holds the new token's K/V at its row -- read from the
-    slice block itself where the block lives in the slice (written back)."""
+@pytest.mark.parametrize("layout,mode,group", [(0, "overlap", 1), (1, "overlap", 1),
+                                               (0, "serial", 2), (1, "overlap", 2)])
+def test_step_runner_append_reaches_every_block(ema, layout, mode, group):
+    """A step with append (either schedule, layer groups of 1 or 2): after one
+    step every sequence's last block, in every layer, holds the new token's K/V
+    at its row -- read from the slice block itself where the block lives in the
+    slice (written back)."""
     from harness import StepRunner
     cfg = synth.LLAMA8B.scaled(layers=4, batch=5)
     w = Workload(cfg, layers=4, lens=[1, 16, 17, 40, 95], slice_layout=layout, fill="device",
-                 frac=0.5)
+                 frac=0.5, group=group, staging_slots=2 * group)
     try:
-        runner = StepRunner(w, "overlap", append=True)
+        runner = StepRunner(w, mode, append=True)
         out = w.new_out()
         runner.run(out)
         torch.cuda.synchronize()
