@@ -506,6 +506,7 @@ def main():
                      "kernel": "paged_decode_attention (attn_mfma_streamk + attn_combine_streamk)"},
         "attention": {"bytes_per_launch": attn_b, "timed_calls": int(at_ms.size),
                       "mean_us": at_mean_s * 1e6,
+                      "tokens_per_s_attention_only": B / (L * at_mean_s),
                       "p10_us": pct(at_ms, 10) * 1e3, "p90_us": pct(at_ms, 90) * 1e3,
                       "GBps": attn_gbps, "frac": attn_gbps / HBM_PEAK_GBPS},
         "prefetch": {"bytes_per_step": float(np.sum(pf_b)), "mean_us": float(pf_ms.mean()) * 1e3,
