@@ -4,11 +4,12 @@
 One step = one decode iteration over every layer of a synthetic paged KV cache
 (Llama-3-8B-shaped by default: 32 layers, 32/8 heads, head dim 128, bf16,
 block 16, batch 64, lengths U[1024, 4096], 30 % of each layer's blocks in the
-slice). Per layer, the slice-resident blocks are prefetched into a staging
-area and paged decode attention reads them from there. Two schedules:
-``--mode serial`` (the default) runs each layer's prefetch and attention on one
-stream; ``--mode overlap`` prefetches layer l+1 on a second stream while
-attention of layer l runs, with ``--slots`` staging slots. On one GPU the slice
+slice). Per layer group (``--group`` consecutive layers, 4 by default), one
+call prefetches the group's slice-resident blocks into a staging area, and
+paged decode attention of each of its layers reads them from there. Two
+schedules: ``--mode serial`` (the default) runs prefetches and attention on
+one stream; ``--mode overlap`` runs the prefetches on a second stream, ahead of
+attention by up to ``--slots`` / ``--group`` − 1 groups. On one GPU the slice
 shares the HBM with attention, so both schedules are bound by the same bytes;
 the other schedule's steps are timed after the headline ones and reported as
 ``alt_mode``. ``--append`` also stores a new token per sequence before each
@@ -64,8 +65,8 @@ def parse():
                     choices=["llama3-8b-kv", "llama-70b-tp8-share", "bursty-8b", "stress",
                              "slab-sweep"])
     ap.add_argument("--mode", default="serial", choices=["serial", "overlap"],
-                    help="serial: prefetch then attention on one stream; overlap: prefetch of "
-                         "layer l+1 on a second stream during attention of layer l")
+                    help="serial: prefetches and attention on one stream; overlap: prefetches "
+                         "on a second stream, ahead of attention")
     ap.add_argument("--no-alt-mode", action="store_true",
                     help="skip the steps in the other mode that are reported alongside")
     ap.add_argument("--group", type=int, default=4,

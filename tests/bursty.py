@@ -9,11 +9,12 @@ Every step, in this order:
      f <- clip(f + U(-0.1, 0.1), 0, fmax), and blocks migrate local <-> slice
      (allocate, copy, free) toward round(f * T), as far as free space allows;
   3. the staging lists and attention tables are rebuilt and one full decode
-     step runs (per layer: prefetch of the next layer's slice blocks
-     overlapped with attention), timed with events.
+     step runs (prefetch per layer group, attention per layer, in the chosen
+     schedule), timed with events.
 
 Pools: the slice holds ceil((fmax + slack) * T) slots, the local pool
-local_frac * T blocks plus two layers of staging (T = blocks of all layers).
+local_frac * T blocks plus two layer groups of staging (T = blocks of all
+layers).
 With local_frac = 1 the borrower can hold everything locally and a reclaim
 never preempts; below 1, a large reclaim at a low slice fraction finds too
 little room for write-back and preempts sequences.

@@ -3,10 +3,10 @@
 A ``Workload`` owns one slice handle sized for the config: every logical
 block of every layer allocated (local or slice per the seeded placement, in a
 seeded random order so physical ids are scattered), ``staging_slots`` layers'
-worth of STAGING local blocks as the prefetch double buffer, and device copies
-of the canonical tables, per-layer prefetch lists and per-layer attention
-tables (canonical with each slice id replaced by the staging block it is
-prefetched into).
+worth of STAGING local blocks that the prefetches fill, and device copies of
+the canonical tables, the prefetch lists (per layer and per layer group) and
+per-layer attention tables (canonical with each slice id replaced by the
+staging block it is prefetched into).
 
 Values: ``fill="host"`` draws every pool element on the host (iid N(0,1)
 rounded to 16 bits) and writes NaN into unused tail token slots, keeping a host
