@@ -2,9 +2,11 @@
 //
 // One handle = host bookkeeping (SliceBook) + two separately allocated device
 // pools + library scratch: an identity remap of all unified ids used by
-// reclaim's table rewrite, a kernel error counter, an upload area for reclaim
-// copy lists (with its pinned host staging), and the attention split-K
-// workspace. Scratch grows on demand; growing synchronizes the device.
+// reclaim's table rewrite, a kernel error counter, an upload area for the copy
+// lists that reclaim and run prefetches build on the host (with its pinned
+// host staging; both sized at create for every block once), and the attention
+// split-K workspace, which grows on first use (growing synchronizes the
+// device).
 #include "ema_slice.h"
 
 #include <hip/hip_runtime.h>
@@ -346,12 +348,18 @@ int ema_slice_prefetch_runs(ema_slice_t h, const int32_t* src_first, const int32
   if (engine == EMA_ENGINE_DMA && h->shape.slice_layout != EMA_LAYOUT_ATTN)
     return fail(EMA_ERR_INVAL, "prefetch_runs: the copy engines need the slice in the local layout");
   const int64_t n_total = int64_t(h->book.n_local()) + h->book.n_slice();
-  std::vector<int32_t> src, dst;
+  int64_t blocks = 0;
   for (int32_t r = 0; r < n_runs; ++r) {
     const int64_t a = src_first[r], b = dst_first[r], k = run_blocks[r];
-    if (k < 0 || a < 0 || b < 0 || a + k > n_total || b + k > n_total ||
-        int64_t(src.size()) + k > n_total)
+    if (k < 0 || a < 0 || b < 0 || a + k > n_total || b + k > n_total || blocks + k > n_total)
       return fail(EMA_ERR_INVAL, "prefetch_runs: run out of range");
+    blocks += k;
+  }
+  std::vector<int32_t> src, dst;
+  src.reserve(size_t(blocks));
+  dst.reserve(size_t(blocks));
+  for (int32_t r = 0; r < n_runs; ++r) {
+    const int64_t a = src_first[r], b = dst_first[r], k = run_blocks[r];
     for (int64_t i = 0; i < k; ++i) {
       src.push_back(int32_t(a + i));
       dst.push_back(int32_t(b + i));

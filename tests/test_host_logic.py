@@ -168,3 +168,26 @@ def test_library_reclaim_victim_order_hand_worked():
         assert own_l.tolist() == [4] and own_s.tolist()[:2] == [4, 4]
     finally:
         lib.close()
+
+
+def test_library_run_prefetch_validation_host_only():
+    """Run prefetches expand to block lists that go through the same checks as
+    a prefetch (host-only library: the check runs, no copy)."""
+    lib = LibHostBackend(12, 8, layout=1)
+    ema = lib.ema
+    try:
+        lib.alloc_blocks(ema.POOL_SLICE, [0] * 8)                    # slots 12..19
+        dst = lib.alloc_blocks(ema.POOL_LOCAL, [ema.STAGING] * 4)    # local 0..3
+        ema.slice_prefetch_runs(lib.h, [12, 16], [0, 2], [2, 2])     # valid: 4 blocks
+        bad = [([12], [int(dst[0])], [2], ema.ENGINE_DMA),           # engines need the local layout
+               ([12], [int(dst[0])], [9], ema.ENGINE_KERNEL),        # run past the pool
+               ([12, 13], [0, 0], [1, 1], ema.ENGINE_KERNEL),        # a staging block twice
+               ([0], [int(dst[0])], [1], ema.ENGINE_KERNEL),         # source not a slice block
+               ([12], [0], [-1], ema.ENGINE_KERNEL),                 # negative run
+               ([12], [0], [1], 7)]                                  # unknown engine
+        for s, d, k, eng in bad:
+            with pytest.raises(ema.EmaError) as e:
+                ema.slice_prefetch_runs(lib.h, s, d, k, engine=eng)
+            assert e.value.code == ema.ERR_INVAL, (s, d, k, eng)
+    finally:
+        lib.close()
