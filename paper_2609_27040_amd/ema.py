@@ -3,8 +3,12 @@
 Each function has the C entry point's name without the ``ema_`` prefix and
 passes its arguments straight through: torch tensors as their device address
 (``data_ptr()``), numpy arrays as host pointers, streams as their hipStream_t.
-Every step of the hot path runs in the library's HIP kernels; there is no
-fallback. If the library has not been built this module raises on import.
+Before a pointer goes to an entry point that launches kernels, the binding
+checks that it is a contiguous GPU tensor of the expected type and at least
+the size the call implies (a kernel would dereference a host address or read
+past a short tensor); host-only slices take numpy arrays. Every step of the
+hot path runs in the library's HIP kernels; there is no fallback. If the
+library has not been built this module raises on import.
 """
 import ctypes
 import os
@@ -95,6 +99,61 @@ def _check(rc):
         raise EmaError(rc, _lib.ema_last_error().decode())
 
 
+# Per handle: host-only flag, 16-bit dtype and KV heads, recorded at create,
+# so that the checks below need no library call.
+_HANDLES = {}
+
+
+def _host_only(h):
+    rec = _HANDLES.get(h)
+    if rec is None:
+        return slice_get_info(h)["device"] < 0
+    return rec[0]
+
+
+def _bad(msg):
+    raise EmaError(ERR_INVAL, msg)
+
+
+def _dev(t, name, dtypes, numel=0):
+    """A device-array argument: a contiguous torch tensor on the GPU of one of
+    ``dtypes`` with at least ``numel`` elements. The kernels read whatever the
+    pointer addresses, so a host array or a short tensor is refused here."""
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        _bad(f"{name}: expected a GPU tensor, got {type(t).__name__}")
+    if t.dtype not in dtypes:
+        _bad(f"{name}: dtype {t.dtype} not in {dtypes}")
+    if not t.is_contiguous():
+        _bad(f"{name}: not contiguous")
+    if t.numel() < numel:
+        _bad(f"{name}: {t.numel()} elements, {numel} needed")
+    return t
+
+
+def _i32_dev(t, name, numel=0):
+    import torch
+    return _dev(t, name, (torch.int32,), numel)
+
+
+def _kv16_dev(h, t, name, numel):
+    """16-bit K/V/query data; when the handle's dtype is known, it must match."""
+    import torch
+    rec = _HANDLES.get(h)
+    want = {F16: (torch.float16,), BF16: (torch.bfloat16,)}.get(rec[1]) if rec else None
+    return _dev(t, name, want or (torch.float16, torch.bfloat16, torch.int16), numel)
+
+
+def _ids(h, a, n, name):
+    """Id list: host int32 array for a host-only slice, else a GPU int32 tensor."""
+    if _host_only(h):
+        a = _i32_host(a)
+        if len(a) < n:
+            _bad(f"{name}: {len(a)} ids, {n} needed")
+        return a
+    return _i32_dev(a, name, n)
+
+
 def _ptr(x):
     """Device address of a torch tensor, host address of a numpy array."""
     if x is None:
@@ -126,11 +185,13 @@ def slice_create(num_kv_heads, head_dim, block_size, dtype, slice_layout, local_
     flags = (CREATE_HOST_ONLY if host_only else 0) | (CREATE_CHECKED if checked else 0)
     _check(_lib.ema_slice_create(ctypes.byref(shape), int(local_bytes), int(lent_bytes), flags,
                                  ctypes.byref(h)))
+    _HANDLES[h.value] = (bool(host_only), shape.dtype, int(num_kv_heads))
     return h.value
 
 
 def slice_destroy(h):
     _check(_lib.ema_slice_destroy(h))
+    _HANDLES.pop(h, None)
 
 
 def slice_get_info(h):
@@ -165,24 +226,20 @@ def slice_lend(h, n_blocks):
     return added.value
 
 
+def _copy_call(fn, h, src, dst, n, stream):
+    n = len(src) if n is None else int(n)
+    src, dst = _ids(h, src, n, "source ids"), _ids(h, dst, n, "destination ids")
+    _check(fn(h, _ptr(src), _ptr(dst), n, None if _host_only(h) else _stream(stream)))
+
+
 def slice_prefetch(h, block_ids, dst_block_table, n=None, stream=None):
     """block_ids, dst_block_table: int32 device tensors (numpy arrays for a
     host-only slice)."""
-    n = len(block_ids) if n is None else n
-    host = isinstance(block_ids, np.ndarray)
-    if host:
-        block_ids, dst_block_table = _i32_host(block_ids), _i32_host(dst_block_table)
-    _check(_lib.ema_slice_prefetch(h, _ptr(block_ids), _ptr(dst_block_table), int(n),
-                                   None if host else _stream(stream)))
+    _copy_call(_lib.ema_slice_prefetch, h, block_ids, dst_block_table, n, stream)
 
 
 def slice_migrate(h, src_ids, dst_ids, n=None, stream=None):
-    n = len(src_ids) if n is None else n
-    host = isinstance(src_ids, np.ndarray)
-    if host:
-        src_ids, dst_ids = _i32_host(src_ids), _i32_host(dst_ids)
-    _check(_lib.ema_slice_migrate(h, _ptr(src_ids), _ptr(dst_ids), int(n),
-                                  None if host else _stream(stream)))
+    _copy_call(_lib.ema_slice_migrate, h, src_ids, dst_ids, n, stream)
 
 
 def slice_prefetch_runs(h, src_first, dst_first, run_blocks, engine=0, stream=None):
@@ -197,23 +254,25 @@ def slice_prefetch_runs(h, src_first, dst_first, run_blocks, engine=0, stream=No
 def slice_writeback(h, staging_ids, slice_ids, n=None, stream=None):
     """staging_ids, slice_ids: int32 device tensors (numpy arrays for a
     host-only slice)."""
-    n = len(staging_ids) if n is None else n
-    host = isinstance(staging_ids, np.ndarray)
-    if host:
-        staging_ids, slice_ids = _i32_host(staging_ids), _i32_host(slice_ids)
-    _check(_lib.ema_slice_writeback(h, _ptr(staging_ids), _ptr(slice_ids), int(n),
-                                    None if host else _stream(stream)))
+    _copy_call(_lib.ema_slice_writeback, h, staging_ids, slice_ids, n, stream)
 
 
 def kv_append(h, k_new, v_new, block_table, seq_lens, stream=None):
     """k_new, v_new [B][Hkv][D] (16-bit), block_table int32 [B][max_blocks],
     seq_lens int32 [B] counting the new token: device tensors (numpy arrays
     for a host-only slice)."""
-    host = isinstance(block_table, np.ndarray)
     B = int(block_table.shape[0])
     max_blocks = int(block_table.shape[1]) if block_table.ndim == 2 else 0
+    host = _host_only(h)
     if host:
         block_table, seq_lens = _i32_host(block_table), _i32_host(seq_lens)
+    else:
+        rec = _HANDLES.get(h)
+        row = rec[2] * 128 if rec else 0          # K/V elements per sequence
+        block_table = _i32_dev(block_table, "block_table", B * max_blocks)
+        seq_lens = _i32_dev(seq_lens, "seq_lens", B)
+        k_new = _kv16_dev(h, k_new, "k_new", B * row)
+        v_new = _kv16_dev(h, v_new, "v_new", B * row)
     _check(_lib.ema_kv_append(h, _ptr(k_new), _ptr(v_new), _ptr(block_table), _ptr(seq_lens), B,
                               max_blocks, None if host else _stream(stream)))
 
@@ -228,8 +287,10 @@ def slice_reclaim(h, n_blocks, canon_tables=None, stream=None, caps=None):
     victims = np.empty(max(cap, 1), dtype=np.int32)
     msrc = np.empty(max(cap, 1), dtype=np.int32)
     mdst = np.empty(max(cap, 1), dtype=np.int32)
-    n_entries = 0 if canon_tables is None else canon_tables.numel()
     host_only = info["device"] < 0
+    if canon_tables is not None and not host_only:
+        canon_tables = _i32_dev(canon_tables, "canon_tables")
+    n_entries = 0 if canon_tables is None else canon_tables.numel()
     _check(_lib.ema_slice_reclaim(h, int(n_blocks), _ptr(canon_tables), n_entries,
                                   None if host_only else _stream(stream), ctypes.byref(res),
                                   victims.ctypes.data, cap, msrc.ctypes.data, mdst.ctypes.data,
@@ -243,8 +304,14 @@ def slice_reclaim(h, n_blocks, canon_tables=None, stream=None, caps=None):
 def paged_decode_attention(h, q, block_table, seq_lens, out, scale=0.0, stream=None):
     """q [B][Hq][D] (16-bit), block_table int32 [B][max_blocks], seq_lens int32
     [B], out float32 [B][Hq][D]: device tensors."""
+    import torch
     B, Hq = int(q.shape[0]), int(q.shape[1])
     max_blocks = int(block_table.shape[1]) if block_table.dim() == 2 else 0
+    if not _host_only(h):
+        q = _kv16_dev(h, q, "q", B * Hq * 128)
+        block_table = _i32_dev(block_table, "block_table", B * max_blocks)
+        seq_lens = _i32_dev(seq_lens, "seq_lens", B)
+        out = _dev(out, "out", (torch.float32,), B * Hq * 128)
     _check(_lib.ema_paged_decode_attention(h, _ptr(q), _ptr(block_table), _ptr(seq_lens), B, Hq,
                                            max_blocks, float(scale), _ptr(out), _stream(stream)))
 

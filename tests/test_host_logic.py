@@ -191,3 +191,23 @@ def test_library_run_prefetch_validation_host_only():
             assert e.value.code == ema.ERR_INVAL, (s, d, k, eng)
     finally:
         lib.close()
+
+
+def test_binding_refuses_arrays_the_kernels_could_not_read():
+    """Device entry points take GPU tensors only: the binding refuses host
+    arrays, CPU tensors, other dtypes, non-contiguous views and short inputs
+    before any pointer reaches the library (a kernel would dereference it)."""
+    import torch
+    from paper_2609_27040_amd import ema
+    ok = torch.zeros(8, dtype=torch.int32)                 # right dtype, but on the CPU
+    for bad in (np.zeros(8, np.int32), ok, ok.to(torch.int64), ok[::2]):
+        with pytest.raises(ema.EmaError) as e:
+            ema._i32_dev(bad, "ids", 4)
+        assert e.value.code == ema.ERR_INVAL
+    lib = LibHostBackend(4, 4)
+    try:
+        with pytest.raises(ema.EmaError) as e:                 # host-only: fewer ids than n
+            ema.slice_prefetch(lib.h, np.array([4], np.int32), np.array([0], np.int32), 2)
+        assert e.value.code == ema.ERR_INVAL
+    finally:
+        lib.close()
