@@ -14,13 +14,17 @@ A plain, slow, obviously correct restatement of what the hot path computes:
 * ``invariants``: the properties the paper fixes (exactly-once ownership,
   static-dynamic symmetry after reclaim) plus conservation and the logical
   view of every block.
+* ``sched``: placement of slice units across GPU pairs by Greedy-Least-Loaded
+  (section 5.2, Appendix C) and the cap after bursty preemptions (section 5.3).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s CPU-baseline
 leg may import this package. It shares no code with the HIP library and never
 imports it; the product path never imports this package.
 
 Parity status: attention, layouts and block copies are pinned against
-independent routines (tests/test_oracle_*.py). The reclaim policy details that
+independent routines (tests/test_oracle_*.py); scheduling by hand-worked
+placements and by the competitive bound of Appendix C checked against
+brute-force optima (tests/test_sched.py). The reclaim policy details that
 the paper leaves open (which slots the lender takes back, how the victim is
 chosen, the order of compaction) are pinned only by hand-worked examples and
 the invariants: parity unpinned by the paper for those choices.
