@@ -165,6 +165,8 @@ class Workload:
             self.attn_dev.copy_(a32)
         self.pf_src_dev = [torch.from_numpy(s).to(dev) for s in self.pf_src]
         self.pf_dst_dev = [torch.from_numpy(d).to(dev) for d in self.pf_dst]
+        self.wb_src_dev = [torch.from_numpy(s).to(dev) for s in self.wb_src]
+        self.wb_dst_dev = [torch.from_numpy(d).to(dev) for d in self.wb_dst]
         # one list per layer group (consecutive layers, swapped together)
         g = self.group
         self.groups = [list(range(k, min(self.L, k + g))) for k in range(0, self.L, g)]
@@ -174,13 +176,16 @@ class Workload:
             dst = np.concatenate([self.pf_dst[l] for l in ls]) if ls else np.zeros(0, np.int32)
             self.pf_src_grp.append(src)
             self.pf_dst_grp.append(dst)
+        self.wb_src_grp = [np.concatenate([self.wb_src[l] for l in ls]) for ls in self.groups]
+        self.wb_dst_grp = [np.concatenate([self.wb_dst[l] for l in ls]) for ls in self.groups]
         if g == 1:
             self.pf_src_grp_dev, self.pf_dst_grp_dev = self.pf_src_dev, self.pf_dst_dev
+            self.wb_src_grp_dev, self.wb_dst_grp_dev = self.wb_src_dev, self.wb_dst_dev
         else:
             self.pf_src_grp_dev = [torch.from_numpy(s).to(dev) for s in self.pf_src_grp]
             self.pf_dst_grp_dev = [torch.from_numpy(d).to(dev) for d in self.pf_dst_grp]
-        self.wb_src_dev = [torch.from_numpy(s).to(dev) for s in self.wb_src]
-        self.wb_dst_dev = [torch.from_numpy(d).to(dev) for d in self.wb_dst]
+            self.wb_src_grp_dev = [torch.from_numpy(s).to(dev) for s in self.wb_src_grp]
+            self.wb_dst_grp_dev = [torch.from_numpy(d).to(dev) for d in self.wb_dst_grp]
 
     def _fill_pattern(self):
         """Every 8-byte word of both pools gets a distinct value (its position,
@@ -207,6 +212,11 @@ class Workload:
 
     def append(self, l, k_new, v_new, stream=None):
         ema.kv_append(self.h, k_new, v_new, self.attn_dev[l], self.lens_dev, stream=stream)
+
+    def writeback_group(self, k, stream=None):
+        """The staged copies layer group k's appends modified, back to the slice."""
+        ema.slice_writeback(self.h, self.wb_src_grp_dev[k], self.wb_dst_grp_dev[k],
+                            len(self.wb_src_grp[k]), stream=stream)
 
     def writeback(self, l, stream=None):
         ema.slice_writeback(self.h, self.wb_src_dev[l], self.wb_dst_dev[l], len(self.wb_src[l]),
@@ -264,9 +274,9 @@ class StepRunner:
     S / group − 1 groups ahead of the attention stream (needs S ≥ 2·group).
 
     With ``append``, each layer first stores the new token's K/V (into the
-    staged copy where the block is in the slice) and the modified staged copies
-    are written back on the copy stream after the layer's attention, before
-    the slot is refilled. ``timers`` (optional) maps group index (``"pf"``) or
+    staged copy where the block is in the slice) and, after the group's last
+    attention, the group's modified staged copies are written back on the copy
+    stream (one call per group), before its slots are refilled. ``timers`` (optional) maps group index (``"pf"``) or
     layer (``"at"``) to the event pair recorded around the call; entries
     missing from a map are not timed (every timing event costs device time)."""
 
@@ -326,9 +336,10 @@ class StepRunner:
                 if t:
                     t[1].record(s1)
                 self.ev_at[l].record(s1)
-                if self.kv_new is not None:
-                    s2.wait_event(self.ev_at[l])
-                    w.writeback(l, stream=s2)
+            if self.kv_new is not None:
+                # the group's modified staged copies go back before its slots are refilled
+                s2.wait_event(self.ev_at[groups[u][-1]])
+                w.writeback_group(u, stream=s2)
 
 
 class BlockedTimer:
