@@ -179,6 +179,45 @@ def test_many_short_sequences(ema, impl, batch, hi, hkv, hq):
         w.close()
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_random_configurations(ema, seed):
+    """Seeded random shapes, block sizes, dtypes, slice layouts, slice
+    fractions and length mixes (with the edge lengths 0, 1, bs and bs + 1
+    sprinkled in), through the default matrix-core stream-K path: prefetch
+    bit-exact, attention within the bar."""
+    rng = np.random.default_rng(1000 + seed)
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    hq = hkv * int(rng.choice([1, 2, 4, 8, 16]))
+    bs = int(rng.choice([16, 32, 64, 128, 256]))
+    dtype = str(rng.choice(["f16", "bf16"]))
+    layout = int(rng.integers(2))
+    batch = int(rng.integers(1, 48))
+    lens = rng.integers(0, int(rng.choice([64, 600, 3000])) + 1, batch)
+    for v in (0, 1, bs, bs + 1):
+        lens[int(rng.integers(batch))] = v
+    frac = float(rng.uniform(0.0, 0.9))
+    print(f"random seed={seed} hq={hq} hkv={hkv} bs={bs} {dtype} layout={layout} "
+          f"batch={batch} frac={frac:.2f}", flush=True)
+    cfg = synth.KVConfig("random", 1, hq, hkv, 128, dtype, bs, batch, ("uniform", 0, 0), frac,
+                         2000 + seed)
+    w = Workload(cfg, lens=lens.tolist(), slice_layout=layout, staging_slots=1)
+    try:
+        st = w.oracle_mirror()
+        w.prefetch(0)
+        st.prefetch(w.pf_src[0], w.pf_dst[0])
+        out = w.new_out()
+        w.attention(0, out)
+        torch.cuda.synchronize()
+        assert ema.slice_device_errors(w.h) == 0
+        assert np.array_equal(w.local_view.cpu().numpy(), st.local)
+        got = out.cpu().numpy()
+        ref = oracle_attention(w, st, 0)
+        assert np.all(got[lens == 0] == 0.0)
+        assert rel_err(got, ref) <= TOL, rel_err(got, ref)
+    finally:
+        w.close()
+
+
 def test_staged_and_all_local_tables_give_identical_bits(ema):
     """Local-remote symmetry as a functional property: the same tokens read
     from staging copies or from other local blocks give the same bits."""
