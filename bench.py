@@ -185,7 +185,9 @@ def symmetry(w, out, s, reps, ema, torch):
     canonical local ones). Pass A runs attention over all layers through the
     staged tables, pass B through the all-local tables; passes alternate.
     Layer 0 is prefetched first and its two outputs must match bit for bit.
-    The fresh blocks are freed again at the end."""
+    The timed passes read whatever the staging slots hold (the same bytes and
+    access pattern as a step; only layer 0's values are compared). The fresh
+    blocks are freed again at the end."""
     L = w.L
     sl = w.tables >= w.n_local
     src = w.tables[sl].astype(np.int32)
