@@ -52,6 +52,7 @@ int ema_sched_create(int32_t n_gpus, int32_t slice_units, int64_t cap_window, em
 }
 
 int ema_sched_destroy(ema_sched_t s) try {
+  if (!s) return set_error(EMA_ERR_INVAL, "sched_destroy: NULL handle");
   delete s;
   return EMA_OK;
 } catch (...) {

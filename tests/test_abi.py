@@ -36,3 +36,42 @@ def test_binding_exposes_the_same_names():
     from paper_2609_27040_amd import ema
     for n in declared_functions():
         assert hasattr(ema, n[len("ema_"):]), n
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="library not built")
+def test_every_entry_point_rejects_a_null_handle():
+    """The header's error contract at the boundary itself: a NULL handle (or
+    NULL out-pointer) returns EMA_ERR_INVAL with a message, before anything
+    else is read -- no GPU needed."""
+    from paper_2609_27040_amd import ema
+    lib = ema._lib
+    z = None
+    calls = {
+        "ema_slice_create": (z, 0, 0, 0, z),
+        "ema_slice_destroy": (z,),
+        "ema_slice_get_info": (z, z),
+        "ema_slice_owners": (z, z, z),
+        "ema_slice_alloc_blocks": (z, 0, 0, z, z),
+        "ema_slice_free_blocks": (z, z, 0),
+        "ema_slice_lend": (z, 0, z),
+        "ema_slice_prefetch": (z, z, z, 0, z),
+        "ema_slice_migrate": (z, z, z, 0, z),
+        "ema_slice_writeback": (z, z, z, 0, z),
+        "ema_slice_prefetch_runs": (z, z, z, z, 0, 0, z),
+        "ema_kv_append": (z, z, z, z, z, 0, 0, z),
+        "ema_slice_reclaim": (z, 0, z, 0, z, z, z, 0, z, z, 0),
+        "ema_paged_decode_attention": (z, z, z, z, 0, 0, 0, 0.0, z, z),
+        "ema_slice_device_errors": (z, z),
+        "ema_sched_destroy": (z,),
+        "ema_sched_create": (2, 1, 0, z),
+        "ema_sched_place": (z, 0, 0, 0, 0, z, z),
+        "ema_sched_release": (z, 0, 0, 0),
+        "ema_sched_preempted": (z, 0, 1, 0),
+        "ema_sched_usage": (z, 0, z, z),
+    }
+    declared = set(declared_functions()) - {"ema_last_error"}
+    assert declared == set(calls), declared ^ set(calls)
+    for name, args in calls.items():
+        rc = getattr(lib, name)(*args)
+        assert rc == ema.ERR_INVAL, (name, rc)
+        assert lib.ema_last_error().decode(), name
