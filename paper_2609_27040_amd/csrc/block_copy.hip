@@ -15,6 +15,8 @@
 // slice layout differs from the local one.
 #include "kernels.h"
 
+#include <algorithm>
+
 namespace ema {
 namespace {
 
@@ -243,12 +245,19 @@ __global__ void table_rewrite_kernel(int32_t* __restrict__ tables, int64_t n_ent
 hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32_t* dst,
                              int32_t n, int32_t* err_count, hipStream_t stream) {
   if (n <= 0) return hipSuccess;
-  const int64_t units = int64_t(n) * (pv.block_bytes / kUnitBytes);
-  const int64_t grid = (units + kWaves - 1) / kWaves;
+  const int64_t upb = pv.block_bytes / kUnitBytes;
   const size_t lds = pv.slice_layout == 0 ? 0 : size_t(kWaves) * tile_elems(pv.block_size) * 2;
-  hipLaunchKernelGGL(block_copy_kernel, dim3(unsigned(grid)), dim3(256), lds, stream, pv, src, dst,
-                     n, err_count);
-  return hipGetLastError();
+  // A launch stays below 2^32 work-items: at most 2^24 workgroups of 256.
+  const int64_t max_blocks = std::max<int64_t>(1, (int64_t(1) << 24) * kWaves / upb);
+  for (int64_t b0 = 0; b0 < n; b0 += max_blocks) {
+    const int32_t m = int32_t(std::min<int64_t>(max_blocks, n - b0));
+    const int64_t grid = (int64_t(m) * upb + kWaves - 1) / kWaves;
+    hipLaunchKernelGGL(block_copy_kernel, dim3(unsigned(grid)), dim3(256), lds, stream, pv,
+                       src + b0, dst + b0, m, err_count);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_kv_append(const PoolView& pv, const void* k_new, const void* v_new,
