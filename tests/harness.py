@@ -218,10 +218,6 @@ class Workload:
         ema.slice_writeback(self.h, self.wb_src_grp_dev[k], self.wb_dst_grp_dev[k],
                             len(self.wb_src_grp[k]), stream=stream)
 
-    def writeback(self, l, stream=None):
-        ema.slice_writeback(self.h, self.wb_src_dev[l], self.wb_dst_dev[l], len(self.wb_src[l]),
-                            stream=stream)
-
     def new_token_kv(self, seed=0):
         """One new token's K and V per sequence (device, the cache dtype)."""
         g = torch.Generator(device="cuda")
