@@ -71,6 +71,8 @@ def parse():
                          "on a second stream, ahead of attention")
     ap.add_argument("--no-alt-mode", action="store_true",
                     help="skip the steps in the other mode that are reported alongside")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the graph-captured steps that are reported alongside")
     ap.add_argument("--group", type=int, default=4,
                     help="layers per layer group: one prefetch call per group")
     ap.add_argument("--slots", type=int, default=None,
@@ -259,6 +261,33 @@ def alt_mode_steps(w, out, mode, args, attn_b):
                            for e0, e1 in tm["at"].values()])) * 1e3
     return {"mode": mode, "ms_per_step": ms_step, "tokens_per_s": w.B / (ms_step / 1e3),
             "attention_mean_us": at_us, "attention_GBps": attn_b / at_us / 1e3}
+
+
+def graph_steps(w, out, runner, args):
+    """The one-stream step captured once as a HIP graph and replayed (reported
+    beside the headline: timing events cannot be captured here, so the
+    roofline stays with the eager steps). The replay's output must equal an
+    eager step's bit for bit."""
+    import torch
+    from harness import capture_step
+    log("graph-captured steps for comparison")
+    runner.run(out)
+    torch.cuda.synchronize()
+    ref = out.clone()
+    g = capture_step(runner, out)
+    for _ in range(args.warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    same = bool(torch.equal(out, ref))
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        g.replay()
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    same = same and bool(torch.equal(out, ref))
+    del g
+    return {"ms_per_step": ms_step, "tokens_per_s": w.B / (ms_step / 1e3),
+            "replay_matches_eager": same}
 
 
 def reclaim_phase(w, s, reps, ema, torch):
@@ -495,6 +524,11 @@ def main():
     if not args.no_alt_mode:
         alt = alt_mode_steps(w, out, "overlap" if args.mode == "serial" else "serial",
                              args, attn_b)
+    graph = None
+    if args.mode == "serial" and not args.no_graph:
+        graph = graph_steps(w, out, runner, args)
+        if not graph["replay_matches_eager"]:
+            raise RuntimeError("graph replay differs from the eager step")
 
     traffic = None
     rec = counter_traffic(cfg.name)
@@ -536,6 +570,8 @@ def main():
         res["roofline"]["traffic_source"] = rec.get("note", "counter summary")
     if alt is not None:
         res["alt_mode"] = alt
+    if graph is not None:
+        res["graph"] = graph
 
     if args.symmetry_reps > 0:
         log("symmetry: staged vs all-local tables")

@@ -309,19 +309,22 @@ class StepRunner:
         w, s1, s2 = self.w, self.s1, self.s2
         groups, US, ahead = w.groups, self.unit_slots, self.ahead
         NG = len(groups)
+        two = s2 is not s1            # on one stream, stream order is the dependency
         for u in range(NG):
             if u == 0:
                 # every slot was last read by the previous step's attention
-                s2.wait_event(self.ev_at[w.L - 1])
+                if two:
+                    s2.wait_event(self.ev_at[w.L - 1])
                 for k in range(min(ahead, NG)):
                     self._prefetch(k, timers)
             k = u + ahead
             if k < NG:
-                if k - US >= 0:
+                if k - US >= 0 and two:
                     # group k's slots were read by group k - US
                     s2.wait_event(self.ev_at[groups[k - US][-1]])
                 self._prefetch(k, timers)
-            s1.wait_event(self.ev_pf[u])
+            if two:
+                s1.wait_event(self.ev_pf[u])
             for l in groups[u]:
                 if self.kv_new is not None:
                     w.append(l, *self.kv_new, stream=s1)
@@ -334,8 +337,21 @@ class StepRunner:
                 self.ev_at[l].record(s1)
             if self.kv_new is not None:
                 # the group's modified staged copies go back before its slots are refilled
-                s2.wait_event(self.ev_at[groups[u][-1]])
+                if two:
+                    s2.wait_event(self.ev_at[groups[u][-1]])
                 w.writeback_group(u, stream=s2)
+
+
+def capture_step(runner, out):
+    """One step of a one-stream runner captured as a HIP graph (after warm-up
+    steps, so every workspace already exists). Nothing in the step allocates or
+    clears memory, so the graph holds kernel and copy nodes only."""
+    if runner.s1 is not runner.s2:
+        raise ValueError("only the one-stream schedule is captured")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=runner.s1):
+        runner.run(out)
+    return g
 
 
 class BlockedTimer:

@@ -241,3 +241,37 @@ def test_step_runner_append_reaches_every_block(ema, layout, mode, group):
         assert ema.slice_device_errors(w.h) == 0
     finally:
         w.close()
+
+
+def test_captured_step_replays_match_eager(ema):
+    """The one-stream step (layer groups of 2, with append and write-back)
+    captured as a HIP graph: every replay, with eager work and
+    synchronisations between replays, leaves the same output and the same
+    pools, byte for byte, as an eager step."""
+    from harness import StepRunner, capture_step
+    cfg = synth.LLAMA8B.scaled(layers=4, batch=6)
+    w = Workload(cfg, layers=4, lens=[1, 16, 17, 40, 95, 300], fill="device", frac=0.5,
+                 group=2, staging_slots=4)
+    try:
+        runner = StepRunner(w, "serial", append=True)
+        out = w.new_out()
+        for _ in range(2):
+            runner.run(out)
+        torch.cuda.synchronize()
+        ref_out = out.clone()
+        ref_local, ref_slice = w.local_view.clone(), w.slice_view.clone()
+        g = capture_step(runner, out)
+        other = w.new_out()
+        for rep in range(3):
+            out.zero_()
+            w.attention(rep % w.L, other)                 # eager work between replays
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(out, ref_out), rep
+            assert torch.equal(w.local_view, ref_local), rep
+            assert torch.equal(w.slice_view, ref_slice), rep
+        assert ema.slice_device_errors(w.h) == 0
+        del g
+    finally:
+        w.close()
