@@ -275,13 +275,15 @@ def graph_steps(w, out, runner, args):
     torch.cuda.synchronize()
     ref = out.clone()
     g = capture_step(runner, out)
-    for _ in range(args.warmup):
-        g.replay()
+    with torch.cuda.stream(runner.s1):           # a graph replays on the current stream
+        for _ in range(args.warmup):
+            g.replay()
     torch.cuda.synchronize()
     same = bool(torch.equal(out, ref))
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        g.replay()
+    with torch.cuda.stream(runner.s1):
+        for _ in range(args.steps):
+            g.replay()
     torch.cuda.synchronize()
     ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
     same = same and bool(torch.equal(out, ref))

@@ -305,11 +305,43 @@ class StepRunner:
             t[1].record(self.s2)
         self.ev_pf[k].record(self.s2)
 
+    def ops(self, out):
+        """One step in the one-stream schedule as an ordered list of
+        (kind, index, call): "pf" (group prefetch), "ap" (append), "at"
+        (attention of a layer), "wb" (group write-back). Stream order is the
+        only dependency, so any contiguous run of them can be captured."""
+        from functools import partial
+        w, s = self.w, self.s1
+        groups, ahead = w.groups, self.ahead
+        NG = len(groups)
+        ops = []
+        for u in range(NG):
+            first = range(min(ahead, NG)) if u == 0 else ()
+            nxt = [u + ahead] if u + ahead < NG else []
+            for k in list(first) + nxt:
+                ops.append(("pf", k, partial(w.prefetch_group, k, stream=s)))
+            for l in groups[u]:
+                if self.kv_new is not None:
+                    ops.append(("ap", l, partial(w.append, l, *self.kv_new, stream=s)))
+                ops.append(("at", l, partial(w.attention, l, out, stream=s)))
+            if self.kv_new is not None:
+                ops.append(("wb", u, partial(w.writeback_group, u, stream=s)))
+        return ops
+
     def run(self, out, timers=None):
         w, s1, s2 = self.w, self.s1, self.s2
+        if s2 is s1:
+            for kind, i, call in self.ops(out):
+                t = timers.get(kind, {}).get(i) if timers else None
+                if t:
+                    t[0].record(s1)
+                call()
+                if t:
+                    t[1].record(s1)
+            return
         groups, US, ahead = w.groups, self.unit_slots, self.ahead
         NG = len(groups)
-        two = s2 is not s1            # on one stream, stream order is the dependency
+        two = True
         for u in range(NG):
             if u == 0:
                 # every slot was last read by the previous step's attention
@@ -342,16 +374,25 @@ class StepRunner:
                 w.writeback_group(u, stream=s2)
 
 
-def capture_step(runner, out):
-    """One step of a one-stream runner captured as a HIP graph (after warm-up
-    steps, so every workspace already exists). Nothing in the step allocates or
-    clears memory, so the graph holds kernel and copy nodes only."""
+def capture_ops(runner, ops):
+    """A contiguous run of a one-stream runner's step operations captured as a
+    HIP graph (after warm-up steps, so every workspace already exists; nothing
+    in the step allocates or clears memory, so the graph holds kernel and copy
+    nodes only). None for an empty run."""
     if runner.s1 is not runner.s2:
         raise ValueError("only the one-stream schedule is captured")
+    if not ops:
+        return None
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=runner.s1):
-        runner.run(out)
+        for _, _, call in ops:
+            call()
     return g
+
+
+def capture_step(runner, out):
+    """One whole step of a one-stream runner as a HIP graph."""
+    return capture_ops(runner, runner.ops(out))
 
 
 class BlockedTimer:

@@ -275,3 +275,4 @@ def test_captured_step_replays_match_eager(ema):
         del g
     finally:
         w.close()
+
