@@ -292,6 +292,30 @@ def graph_steps(w, out, runner, args):
             "replay_matches_eager": same}
 
 
+def hbm_context(torch, gib=2, reps=5):
+    """A plain torch device-to-device copy (read + write counted) on this GPU
+    in the same run, as context for the fractions of 8 TB/s."""
+    n = (gib << 30) // 2
+    x = torch.randn(n, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    y = torch.empty_like(x)
+    res = {}
+    for name, fn, nbytes in (("torch_copy_GBps", lambda: y.copy_(x), 4 * n),):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        res[name] = nbytes / (float(np.median(ts)) / 1e3) / 1e9
+    del x, y
+    torch.cuda.empty_cache()
+    return res
+
+
 def reclaim_phase(w, s, reps, ema, torch):
     """The lender takes 5 % of its lent blocks back, ``reps`` times. Each call is
     queued behind a device copy long enough to outlast the call's host planning,
@@ -593,6 +617,8 @@ def main():
     if errs:
         raise RuntimeError(f"kernels skipped {errs} invalid ids")
     w.close()
+    if not args.no_cpu_baseline:                  # the full default run only
+        res["hbm_context"] = hbm_context(torch)
     print(json.dumps(res))
 
 
