@@ -78,7 +78,9 @@ def parse():
     ap.add_argument("--slots", type=int, default=None,
                     help="staging slots, a multiple of the group size (default: two groups)")
     ap.add_argument("--timed-layers", type=int, default=2,
-                    help="layers per step whose calls get timing events (rotating)")
+                    help="with --append: layers per step whose attention calls get their own "
+                         "timing events (rotating); without it each step times one layer "
+                         "group's consecutive attention calls between one event pair")
     ap.add_argument("--append", action="store_true",
                     help="each layer also appends the new token's K/V and writes the modified "
                          "staged blocks back to the slice")
@@ -134,6 +136,36 @@ def counter_traffic(workload):
 
 def pct(a, q):
     return float(np.percentile(np.asarray(a), q))
+
+
+def step_timers(runner, args, k):
+    """Timing events for step k. Without append, one layer group per step
+    (rotating over the groups) gets one event pair around its consecutive
+    attention calls and one around its prefetch: each event packet costs a
+    few microseconds of device time, which a pair per call would add to
+    every timed call. With append, a call's append sits between the
+    attention calls, so a few layers per step are timed call by call."""
+    w = runner.w
+    if runner.kv_new is None:
+        u = k % len(w.groups)
+        return runner.new_timers(layers=[], groups=[u], attn_groups=[u])
+    nt = max(1, min(w.L, args.timed_layers))
+    return runner.new_timers([(nt * k + i) % w.L for i in range(nt)])
+
+
+def attention_samples(timers, w):
+    """Per-call attention times (ms) of every timed unit (a call, or a group's
+    run of calls divided by its length) and the number of calls covered."""
+    per_call, calls = [], 0
+    for tm in timers:
+        for e0, e1 in tm["at"].values():
+            per_call.append(e0.elapsed_time(e1))
+            calls += 1
+        for u, (e0, e1) in tm["atg"].items():
+            n = len(w.groups[u])
+            per_call.append(e0.elapsed_time(e1) / n)
+            calls += n
+    return np.array(per_call), calls
 
 
 def cpu_baseline(w, seconds):
@@ -247,18 +279,14 @@ def alt_mode_steps(w, out, mode, args, attn_b):
     runner = StepRunner(w, mode)
     for _ in range(args.warmup):
         runner.run(out)
-    L = w.L
-    nt = max(1, min(L, args.timed_layers))
-    timers = [runner.new_timers([(nt * k + i) % L for i in range(nt)])
-              for k in range(args.steps)]
+    timers = [step_timers(runner, args, k) for k in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
         runner.run(out, timers[k])
     torch.cuda.synchronize()
     ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
-    at_us = float(np.mean([e0.elapsed_time(e1) for tm in timers
-                           for e0, e1 in tm["at"].values()])) * 1e3
+    at_us = float(attention_samples(timers, w)[0].mean()) * 1e3
     return {"mode": mode, "ms_per_step": ms_step, "tokens_per_s": w.B / (ms_step / 1e3),
             "attention_mean_us": at_us, "attention_GBps": attn_b / at_us / 1e3}
 
@@ -521,11 +549,9 @@ def main():
     for _ in range(args.warmup):
         runner.run(out)
     torch.cuda.synchronize()
-    # every timing event costs device time, so each step times a few layers
-    # (rotating over the steps) and the rest run without events
-    nt = max(1, min(L, args.timed_layers))
-    timers = [runner.new_timers([(nt * k + i) % L for i in range(nt)])
-              for k in range(args.steps)]
+    # every timing event costs device time, so each step times one layer
+    # group (rotating over the steps) and the rest run without events
+    timers = [step_timers(runner, args, k) for k in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -537,7 +563,7 @@ def main():
     if errs:
         raise RuntimeError(f"kernels skipped {errs} invalid ids")
 
-    at_ms = np.array([e0.elapsed_time(e1) for tm in timers for e0, e1 in tm["at"].values()])
+    at_ms, at_calls = attention_samples(timers, w)
     pf_ms = np.array([e0.elapsed_time(e1) for tm in timers for e0, e1 in tm["pf"].values()])
     pf_timed_b = float(sum(pf_b[k] for tm in timers for k in tm["pf"]))
     at_mean_s = float(at_ms.mean()) / 1e3
@@ -582,7 +608,10 @@ def main():
         "roofline": {"bound": "hbm", "achieved": attn_gbps, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": attn_gbps / HBM_PEAK_GBPS, "traffic": traffic,
                      "kernel": "paged_decode_attention (attn_mfma_streamk + attn_combine_streamk)"},
-        "attention": {"bytes_per_launch": attn_b, "timed_calls": int(at_ms.size),
+        "attention": {"bytes_per_launch": attn_b, "timed_calls": int(at_calls),
+                      "timing": ("one event pair per call" if args.append else
+                                 f"one event pair around each timed group's {w.group} "
+                                 "consecutive calls"),
                       "mean_us": at_mean_s * 1e6,
                       "tokens_per_s_attention_only": B / (L * at_mean_s),
                       "p10_us": pct(at_ms, 10) * 1e3, "p90_us": pct(at_ms, 90) * 1e3,

@@ -272,9 +272,13 @@ class StepRunner:
     With ``append``, each layer first stores the new token's K/V (into the
     staged copy where the block is in the slice) and, after the group's last
     attention, the group's modified staged copies are written back on the copy
-    stream (one call per group), before its slots are refilled. ``timers`` (optional) maps group index (``"pf"``) or
-    layer (``"at"``) to the event pair recorded around the call; entries
-    missing from a map are not timed (every timing event costs device time)."""
+    stream (one call per group), before its slots are refilled.
+
+    ``timers`` (optional) maps group index (``"pf"``) or layer (``"at"``) to
+    the event pair recorded around that call, and group index (``"atg"``) to
+    one event pair around the group's consecutive attention calls (steps
+    without append only); entries missing from a map are not timed (every
+    timing event costs device time)."""
 
     def __init__(self, w, mode="overlap", append=False):
         self.w = w
@@ -289,12 +293,26 @@ class StepRunner:
         self.ev_pf = [torch.cuda.Event() for _ in range(len(w.groups))]
         self.ev_at = [torch.cuda.Event() for _ in range(w.L)]
 
-    def new_timers(self, layers=None, groups=None):
+    def new_timers(self, layers=None, groups=None, attn_groups=()):
         mk = lambda: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
         layers = range(self.w.L) if layers is None else layers
+        if attn_groups and self.kv_new is not None:
+            raise ValueError("group attention timers need steps without append")
         if groups is None:
-            groups = sorted({l // self.w.group for l in layers})
-        return {"pf": {k: mk() for k in groups}, "at": {l: mk() for l in layers}}
+            groups = sorted({l // self.w.group for l in layers} | set(attn_groups))
+        return {"pf": {k: mk() for k in groups}, "at": {l: mk() for l in layers},
+                "atg": {u: mk() for u in attn_groups}}
+
+    def _attn_timer(self, l, timers):
+        """(event pair, record before, record after) for layer l's attention."""
+        if not timers:
+            return None, False, False
+        t = timers["at"].get(l)
+        if t:
+            return t, True, True
+        grp = self.w.groups[l // self.w.group]
+        t = timers.get("atg", {}).get(l // self.w.group)
+        return t, bool(t) and l == grp[0], bool(t) and l == grp[-1]
 
     def _prefetch(self, k, timers):
         t = timers["pf"].get(k) if timers else None
@@ -332,11 +350,15 @@ class StepRunner:
         w, s1, s2 = self.w, self.s1, self.s2
         if s2 is s1:
             for kind, i, call in self.ops(out):
-                t = timers.get(kind, {}).get(i) if timers else None
-                if t:
+                if kind == "at":
+                    t, before, after = self._attn_timer(i, timers)
+                else:
+                    t = timers.get(kind, {}).get(i) if timers else None
+                    before = after = bool(t)
+                if before:
                     t[0].record(s1)
                 call()
-                if t:
+                if after:
                     t[1].record(s1)
             return
         groups, US, ahead = w.groups, self.unit_slots, self.ahead
@@ -360,11 +382,11 @@ class StepRunner:
             for l in groups[u]:
                 if self.kv_new is not None:
                     w.append(l, *self.kv_new, stream=s1)
-                t = timers["at"].get(l) if timers else None
-                if t:
+                t, before, after = self._attn_timer(l, timers)
+                if before:
                     t[0].record(s1)
                 w.attention(l, out, stream=s1)
-                if t:
+                if after:
                     t[1].record(s1)
                 self.ev_at[l].record(s1)
             if self.kv_new is not None:

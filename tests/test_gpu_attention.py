@@ -131,6 +131,37 @@ def test_long_sequences_many_splits(ema, impl, hq, hkv, bs, dtype, lens):
         w.close()
 
 
+def test_calls_with_different_cuts_on_one_handle(ema, impl):
+    """Successive calls on one handle whose stream-K ranges cut different
+    (sequence, KV head) pairs into different numbers of pieces (batch and
+    lengths change between calls): the reused partial slots and merge records
+    must never carry a previous call's pieces into the next."""
+    print(f"rearm {impl}", flush=True)
+    rng = np.random.default_rng(313)
+    lens_a = rng.integers(200, 6000, 24)
+    cfg = synth.KVConfig("rearm", 1, 8, 1, 128, "bf16", 32, 24, ("uniform", 0, 0), 0.5, 313)
+    w = Workload(cfg, lens=lens_a.tolist(), staging_slots=1)
+    try:
+        st = w.oracle_mirror()
+        w.prefetch(0)
+        st.prefetch(w.pf_src[0], w.pf_dst[0])
+        cases = [(24, lens_a), (24, lens_a // 3), (10, lens_a[:10]), (24, lens_a[::-1] % 700),
+                 (24, lens_a)]
+        for k, (nb, lens) in enumerate(cases):
+            lens = np.minimum(lens, lens_a[:nb]).astype(np.int64)
+            out = torch.full((nb, 8, 128), float("nan"), device="cuda")
+            ema.paged_decode_attention(w.h, w.q[:nb], w.attn_dev[0][:nb],
+                                       torch.as_tensor(lens.astype(np.int32), device="cuda"), out)
+            torch.cuda.synchronize()
+            got = out.cpu().numpy()
+            ref = oracle.paged_decode_attention(w.q16[:nb], w.attn_tables[0][:nb], lens,
+                                                st.read_block, w.hkv, w.D, w.bs, w.cfg.dtype)
+            assert rel_err(got, ref) <= TOL, (k, rel_err(got, ref))
+        assert ema.slice_device_errors(w.h) == 0
+    finally:
+        w.close()
+
+
 def test_wide_batch_takes_the_long_chunk_path(ema, impl):
     """batch x kv heads >= 256 selects 512-token workgroups; full oracle check."""
     print(f"wide {impl}", flush=True)
