@@ -14,8 +14,9 @@ shares the HBM with attention, so both schedules are bound by the same bytes;
 the other schedule's steps are timed after the headline ones and reported as
 ``alt_mode``. ``--append`` also stores a new token per sequence before each
 layer's attention and writes the modified staged blocks back to the slice
-after it. Each step times a few layers' calls with events (rotating), since
-every event costs device time.
+after it. Every event costs device time, so each step times one layer group
+(rotating): one event pair around its prefetch and one around its
+consecutive attention calls (with ``--append``, two layers' calls one by one).
 
 After the timed steps, untimed by the step clock:
   * symmetry: attention over every layer through the staged tables versus
@@ -31,8 +32,8 @@ After the timed steps, untimed by the step clock:
 Prints one JSON line. ``value`` is decode tokens/s of the whole step
 (batch / step time; attention only, no projections or MLP). The roofline
 object is for the attention entry point (its kernels' algorithmic HBM bytes
-over their mean duration, from HIP events on the attention stream during the
-timed steps); its ``traffic`` comes from the committed counter summary of the
+over their mean duration per call, from HIP events on the attention stream
+during the timed steps); its ``traffic`` comes from the committed counter summary of the
 same workload and is null when the kernel sources no longer match it.
 """
 import argparse

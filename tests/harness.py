@@ -363,22 +363,19 @@ class StepRunner:
             return
         groups, US, ahead = w.groups, self.unit_slots, self.ahead
         NG = len(groups)
-        two = True
         for u in range(NG):
             if u == 0:
                 # every slot was last read by the previous step's attention
-                if two:
-                    s2.wait_event(self.ev_at[w.L - 1])
+                s2.wait_event(self.ev_at[w.L - 1])
                 for k in range(min(ahead, NG)):
                     self._prefetch(k, timers)
             k = u + ahead
             if k < NG:
-                if k - US >= 0 and two:
+                if k - US >= 0:
                     # group k's slots were read by group k - US
                     s2.wait_event(self.ev_at[groups[k - US][-1]])
                 self._prefetch(k, timers)
-            if two:
-                s1.wait_event(self.ev_pf[u])
+            s1.wait_event(self.ev_pf[u])
             for l in groups[u]:
                 if self.kv_new is not None:
                     w.append(l, *self.kv_new, stream=s1)
@@ -391,8 +388,7 @@ class StepRunner:
                 self.ev_at[l].record(s1)
             if self.kv_new is not None:
                 # the group's modified staged copies go back before its slots are refilled
-                if two:
-                    s2.wait_event(self.ev_at[groups[u][-1]])
+                s2.wait_event(self.ev_at[groups[u][-1]])
                 w.writeback_group(u, stream=s2)
 
 
