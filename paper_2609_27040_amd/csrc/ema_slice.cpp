@@ -561,8 +561,8 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
       }
     }
   }
-  // Scheduling. Matrix-core kernel: stream-K (equal tile ranges per resident
-  // workgroup, at most two partials each) when the batch fits its LDS work
+  // Scheduling. Matrix-core kernel: stream-K (equal tile ranges, one
+  // workgroup per CU, at most two partials each) when the batch fits its LDS work
   // list, else a grid of 1024-token chunks. Vector-ALU kernel: a grid of
   // 256-token chunks. Grid forms keep one partial per (sequence, head, chunk).
   const int64_t tiles = int64_t(batch) * hkv * ((max_tokens + 31) / 32);

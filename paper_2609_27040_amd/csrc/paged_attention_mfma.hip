@@ -18,15 +18,18 @@
 //            P is split into a 16-bit high part and a 16-bit remainder so the
 //            probabilities keep ~16 significant bits)
 // Scheduling is stream-K: the tiles of all (sequence, KV head) pairs, in that
-// order, are split into equal contiguous ranges, one per resident workgroup
-// (4 wavefronts), so every workgroup streams the same number of bytes
+// order, are split into equal contiguous ranges, one per workgroup of 4
+// wavefronts and one workgroup per CU, so every CU streams the same bytes
 // whatever the length mix. A workgroup keeps its softmax state across the
 // tiles of one (sequence, KV head); a pair it covers whole is written out
 // directly, a pair cut by a range boundary leaves one partial per workgroup
 // (unnormalised output, max, sum) that a small combine kernel merges. Merging
-// in-kernel would need device-scope fences, which write back and invalidate an
-// XCD's whole L2 per workgroup on this chip. Masked tokens (past the length, or in a block whose id is out of
-// range) get -inf scores and zeroed V, so NaN in unused slots never leaks.
+// inside this kernel costs more: partials must cross XCDs, whose L2s are not
+// coherent, either behind device-scope fences (a whole-L2 write-back and
+// invalidation per workgroup) or as written-through stores plus an arrival
+// counter, and either way at the end of every workgroup's range. Masked tokens
+// (past the length, or in a block whose id is out of range) get -inf scores
+// and zeroed V, so NaN in unused slots never leaks.
 // Reduction orders depend only on sequence lengths, not on block ids.
 #include "kernels.h"
 
@@ -49,11 +52,12 @@ constexpr int kPieceTiles = 32;            // tiles whose block ids are staged i
 constexpr int kMaxIds = kPieceTiles * kIt / 16;
 constexpr int kMaxPersistBatch = 2048;     // sequences the stream-K work list holds in LDS
 constexpr int kGridChunkTiles = 32;        // tiles per workgroup in the grid fallback
-// Starting a (sequence, KV head) costs a workgroup about five tiles' time (its
+// Starting a (sequence, KV head) costs a workgroup several tiles' time (its
 // pipeline drains and refills, the four wavefronts merge, a partial is
-// written), measured on 32-token tiles; the stream-K split counts it so that
-// workgroups that touch more pairs get fewer tiles.
-constexpr int kSegCost = 5;
+// written); the stream-K split counts it as kSegCost tiles so that workgroups
+// that touch more pairs get fewer tiles (measured best between 5 and 8 on
+// 32-token tiles with one workgroup per CU).
+constexpr int kSegCost = 8;
 
 __device__ __forceinline__ u32x4 ld16(const char* p) {
   return *reinterpret_cast<const u32x4*>(p);
@@ -521,21 +525,22 @@ __global__ __launch_bounds__(kThreads) void attn_combine_streamk(AttnArgs a) {
   a.out[(int64_t(b) * a.q_heads + kvh * G + g) * kD + d] = L > 0.0f ? O / L : 0.0f;
 }
 
-template <typename K>
-int resident_workgroups(K kernel) {
-  int dev = 0, cus = 0, per_cu = 0;
+// Stream-K grid: one workgroup per CU. A second resident workgroup per CU
+// adds no bandwidth (the two share the CU's memory path, the second running
+// about 20 % slower) but doubles the cut pairs and their partials.
+int streamk_grid() {
+  int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0) != hipSuccess)
-    return 0;
-  return cus * (per_cu > 0 ? per_cu : 1);
+      cus <= 0)
+    return 256;
+  return std::min(cus, kMaxStreamGrid);
 }
 
 template <int G, int BS, bool BF16>
 hipError_t launch_typed(const AttnArgs& a, hipStream_t stream) {
   if (a.stream_k) {
-    static const int resident = resident_workgroups(attn_mfma_streamk<G, BS, BF16>);
-    const int grid = std::max(1, std::min(resident > 0 ? resident : 512, kMaxStreamGrid));
+    static const int grid = streamk_grid();
     hipLaunchKernelGGL((attn_mfma_streamk<G, BS, BF16>), dim3(grid), dim3(kThreads), 0, stream,
                        a);
     hipError_t e = hipGetLastError();
