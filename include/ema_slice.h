@@ -33,6 +33,8 @@
  *   there) leaves that bookkeeping in place.
  *   Pointers marked "device" are HIP device pointers owned by the caller;
  *   "host" pointers are ordinary memory. The library owns both pools.
+ *   Entry points make the handle's device current while they run and give
+ *   the caller's current device back before returning.
  *   `stream` is a hipStream_t (NULL = the null stream). Kernels are enqueued
  *   asynchronously; host bookkeeping changes at call time. Ordering across
  *   streams is the caller's job (events).

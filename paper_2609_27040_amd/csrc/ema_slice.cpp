@@ -16,6 +16,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <exception>
+#include <memory>
 #include <new>
 #include <string>
 #include <vector>
@@ -110,12 +111,29 @@ ema::PoolView pool_view(const ema_slice* h) {
   return pv;
 }
 
-int use_device(const ema_slice* h) {
-  int cur = -1;
-  HIP_TRY(hipGetDevice(&cur), "hipGetDevice");
-  if (cur != h->device) HIP_TRY(hipSetDevice(h->device), "hipSetDevice");
-  return EMA_OK;
-}
+// Makes the handle's device current for the rest of an entry point and puts
+// the caller's device back when the entry point returns.
+class DeviceScope {
+ public:
+  DeviceScope() = default;
+  DeviceScope(const DeviceScope&) = delete;
+  DeviceScope& operator=(const DeviceScope&) = delete;
+  ~DeviceScope() {
+    if (prev_ >= 0) (void)hipSetDevice(prev_);
+  }
+  int enter(const ema_slice* h) {
+    int cur = -1;
+    HIP_TRY(hipGetDevice(&cur), "hipGetDevice");
+    if (cur != h->device) {
+      HIP_TRY(hipSetDevice(h->device), "hipSetDevice");
+      prev_ = cur;
+    }
+    return EMA_OK;
+  }
+
+ private:
+  int prev_ = -1;
+};
 
 // Reads n ints of a device array to the host (checked mode).
 int fetch_ints(const int32_t* dev, int64_t n, hipStream_t st, std::vector<int32_t>* out) {
@@ -176,7 +194,10 @@ int ema_slice_create(const ema_kv_shape* shape, size_t local_bytes, size_t lent_
   const uint64_t nl = local_bytes / uint64_t(bb), ns = lent_bytes / uint64_t(bb);
   if (nl + ns >= (1ull << 31)) return fail(EMA_ERR_INVAL, "create: more than 2^31 blocks");
 
-  ema_slice* h = new ema_slice;
+  // Owned here until the handle is complete: an exception on the way (host
+  // memory) releases it.
+  std::unique_ptr<ema_slice, void (*)(ema_slice*)> guard(new ema_slice, release);
+  ema_slice* h = guard.get();
   h->shape = *shape;
   h->bb = bb;
   h->host_only = (flags & EMA_CREATE_HOST_ONLY) != 0;
@@ -187,7 +208,7 @@ int ema_slice_create(const ema_kv_shape* shape, size_t local_bytes, size_t lent_
   h->attn_grid = sched && std::strcmp(sched, "grid") == 0;
   h->book.init(int32_t(nl), int32_t(ns));
   if (h->host_only) {
-    *out = h;
+    *out = guard.release();
     return EMA_OK;
   }
   hipError_t e = hipGetDevice(&h->device);
@@ -207,12 +228,8 @@ int ema_slice_create(const ema_kv_shape* shape, size_t local_bytes, size_t lent_
   if (e == hipSuccess) e = hipMalloc(&h->d_work, work * 4);
   if (e == hipSuccess) h->work_cap = work;
   if (e == hipSuccess) e = hipDeviceSynchronize();
-  if (e != hipSuccess) {
-    const int rc = hip_fail(e, "create");
-    release(h);
-    return rc;
-  }
-  *out = h;
+  if (e != hipSuccess) return hip_fail(e, "create");   // the guard releases h
+  *out = guard.release();
   return EMA_OK;
 } catch (...) {
   return internal_error();
@@ -221,7 +238,8 @@ int ema_slice_create(const ema_kv_shape* shape, size_t local_bytes, size_t lent_
 int ema_slice_destroy(ema_slice_t h) try {
   if (!h) return fail(EMA_ERR_INVAL, "destroy: NULL handle");
   if (!h->host_only) {
-    int rc = use_device(h);
+    DeviceScope ds;
+    int rc = ds.enter(h);
     if (rc) return rc;
   }
   release(h);
@@ -310,7 +328,8 @@ static int copy_entry(ema_slice_t h, const int32_t* src, const int32_t* dst, int
     return rc ? fail(rc, err) : EMA_OK;
   }
   if (n == 0) return EMA_OK;
-  int rc = use_device(h);
+  DeviceScope ds;
+  int rc = ds.enter(h);
   if (rc) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (h->checked) {
@@ -370,7 +389,8 @@ int ema_slice_prefetch_runs(ema_slice_t h, const int32_t* src_first, const int32
   int rc = h->book.check_prefetch(src.data(), dst.data(), n, &err);
   if (rc) return fail(rc, err);
   if (h->host_only || n == 0) return EMA_OK;
-  if ((rc = use_device(h))) return rc;
+  DeviceScope ds;
+  if ((rc = ds.enter(h))) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (engine == EMA_ENGINE_DMA) {
     const ema::PoolView pv = pool_view(h);
@@ -430,7 +450,8 @@ int ema_kv_append(ema_slice_t h, const void* k_new, const void* v_new, const int
   };
   if (h->host_only) return batch ? check(seq_lens, block_table) : EMA_OK;
   if (batch == 0) return EMA_OK;
-  int rc = use_device(h);
+  DeviceScope ds;
+  int rc = ds.enter(h);
   if (rc) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (h->checked) {
@@ -458,7 +479,8 @@ int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, in
   if (h->host_only && (canon_tables || n_entries))
     return fail(EMA_ERR_INVAL, "reclaim: host-only slices take no device tables");
   int rc;
-  if (!h->host_only && (rc = use_device(h))) return rc;
+  DeviceScope ds;
+  if (!h->host_only && (rc = ds.enter(h))) return rc;
 
   ema::ReclaimPlan plan;
   std::string err;
@@ -542,7 +564,8 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
   if (max_tokens > (1LL << 30)) return fail(EMA_ERR_INVAL, "attention: max_blocks too large");
   if (h->host_only || batch == 0) return EMA_OK;
   if (h->book.n_local() == 0) return fail(EMA_ERR_INVAL, "attention: the local pool is empty");
-  int rc = use_device(h);
+  DeviceScope ds;
+  int rc = ds.enter(h);
   if (rc) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (h->checked) {
@@ -617,7 +640,8 @@ int ema_slice_device_errors(ema_slice_t h, int32_t* count) try {
   if (!h || !count) return fail(EMA_ERR_INVAL, "device_errors: NULL argument");
   *count = 0;
   if (h->host_only) return EMA_OK;
-  int rc = use_device(h);
+  DeviceScope ds;
+  int rc = ds.enter(h);
   if (rc) return rc;
   HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize");
   HIP_TRY(hipMemcpy(count, h->d_err, 4, hipMemcpyDeviceToHost), "hipMemcpy(err)");
