@@ -21,7 +21,8 @@
 // order, are split into equal contiguous ranges, one per workgroup of 4
 // wavefronts and one workgroup per CU, so every CU streams the same bytes
 // whatever the length mix. A workgroup keeps its softmax state across the
-// tiles of one (sequence, KV head); a pair it covers whole is written out
+// tiles of one (sequence, KV head) and issues the first loads of its next
+// pair before merging the current one; a pair it covers whole is written out
 // directly, a pair cut by a range boundary leaves one partial per workgroup
 // (unnormalised output, max, sum) that a small combine kernel merges. Merging
 // inside this kernel costs more: partials must cross XCDs, whose L2s are not
@@ -52,12 +53,19 @@ constexpr int kPieceTiles = 32;            // tiles whose block ids are staged i
 constexpr int kMaxIds = kPieceTiles * kIt / 16;
 constexpr int kMaxPersistBatch = 2048;     // sequences the stream-K work list holds in LDS
 constexpr int kGridChunkTiles = 32;        // tiles per workgroup in the grid fallback
-// Starting a (sequence, KV head) costs a workgroup several tiles' time (its
-// pipeline drains and refills, the four wavefronts merge, a partial is
-// written); the stream-K split counts it as kSegCost tiles so that workgroups
-// that touch more pairs get fewer tiles (measured best between 5 and 8 on
-// 32-token tiles with one workgroup per CU).
+// Each (sequence, KV head) a workgroup touches costs it several tiles' time
+// (the four wavefronts merge and a partial is written; without the staged
+// range below, the tile pipeline also drains and refills); the stream-K split
+// counts it as kSegCost tiles so that workgroups that touch more pairs get
+// fewer tiles (measured best between 6 and 10 on 32-token tiles with one
+// workgroup per CU).
 constexpr int kSegCost = 8;
+// A stream-K range whose segments and block ids fit these bounds is staged
+// in LDS up front, so each segment can start while the previous one merges.
+constexpr int kMaxSegMax = 8;              // segments of a range (4 for G = 16)
+template <int G>
+constexpr int max_seg() { return G >= 16 ? 4 : kMaxSegMax; }
+constexpr int kRangeIds = 512;             // block ids of a range
 
 __device__ __forceinline__ u32x4 ld16(const char* p) {
   return *reinterpret_cast<const u32x4*>(p);
@@ -311,6 +319,117 @@ __device__ __forceinline__ void attend_segment(const AttnArgs& a, int b, int kvh
 // Workgroup-uniform value kept in a scalar register.
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// One segment of a stream-K range: tiles [j0, j1) of (sequence b, KV head
+// kvh); id0 is the index of its first block id in the range's staged list.
+struct SegDesc {
+  int b, kvh, len, j0, j1, id0;
+};
+
+// Q^T of segment s from its LDS copy (rows past G read as zero).
+template <int G>
+__device__ __forceinline__ void load_q(u32x4 (&qb)[4], const uint16_t (*sq)[G][kD], int s, int r16,
+                                       int q4) {
+  const uint16_t* row = sq[s][r16 < G ? r16 : 0] + q4 * 8;
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(row + kk * 32);
+    qb[kk] = r16 < G ? v : u32x4{0, 0, 0, 0};
+  }
+}
+
+// All segments of a stream-K range with their block ids already in LDS: the
+// four waves stream tiles as in attend_segment, and each wave issues the loads
+// of its first tile of the next segment (and the next segment's queries)
+// before the merge of the current one, so no segment starts from an empty
+// pipeline.
+template <int G, int BS, bool BF16, typename Emit>
+__device__ __forceinline__ void attend_range(const AttnArgs& a, const SegDesc* sd, int nseg,
+                                             const int32_t* ids, const uint16_t (*sq)[G][kD],
+                                             Smem<G>& sm, Emit&& emit) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int r16 = lane & 15;
+  const int q4 = lane >> 4;
+  const char* pool = a.local;
+  const int64_t Bb = a.block_bytes;
+  auto n_tiles = [&](int s) {
+    const int nt = sd[s].j1 - sd[s].j0;
+    return nt > wave ? (nt - wave + kWaves - 1) / kWaves : 0;
+  };
+  auto load_at = [&](Tile& T, int s, int k) {
+    const int j0 = uniform(sd[s].j0);
+    load_tile<BS>(T, (j0 + wave + k * kWaves) * kIt, uniform(sd[s].len), j0 * kIt / BS,
+                  ids + uniform(sd[s].id0), pool, Bb, uniform(sd[s].kvh), r16, q4);
+  };
+  u32x4 qb[4];
+  Tile A, B;
+  if (nseg > 0) {
+    load_q<G>(qb, sq, 0, r16, q4);
+    if (n_tiles(0) > 0) load_at(A, 0, 0);
+  }
+  for (int s = 0; s < nseg; ++s) {
+    const int n_it = n_tiles(s);
+    const bool has_next = s + 1 < nseg && n_tiles(s + 1) > 0;
+    bool issued_next = false;
+    float m = -INFINITY;
+    float lsum = 0.0f;
+    f32x4 o[8];
+#pragma unroll
+    for (int n = 0; n < 8; ++n) o[n] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int it = 0; it < n_it; it += 2) {
+      consume_tile<BF16>(A, qb, a.scale_log2, m, lsum, o, [&] {
+        if (it + 1 < n_it) load_at(B, s, it + 1);
+      });
+      if (it + 1 >= n_it) break;
+      consume_tile<BF16>(B, qb, a.scale_log2, m, lsum, o, [&] {
+        if (it + 2 < n_it) {
+          load_at(A, s, it + 2);
+        } else if (has_next) {
+          load_at(A, s + 1, 0);
+          issued_next = true;
+        }
+      });
+    }
+    if (has_next && !issued_next) load_at(A, s + 1, 0);
+    if (s + 1 < nseg) load_q<G>(qb, sq, s + 1, r16, q4);
+
+    // ---- merge the four waves (as in attend_segment) ----
+    __syncthreads();                       // the previous merge is read out
+    lsum += __shfl_xor(lsum, 16);
+    lsum += __shfl_xor(lsum, 32);
+    if (r16 < G) {
+      if (q4 == 0) {
+        sm.m[wave][r16] = m;
+        sm.l[wave][r16] = lsum;
+      }
+#pragma unroll
+      for (int n = 0; n < 8; ++n)
+        *reinterpret_cast<f32x4*>(&sm.o[wave][r16][16 * n + 4 * q4]) = o[n];
+    }
+    __syncthreads();
+    for (int e = tid; e < G * kD; e += kThreads) {
+      const int g = e / kD;
+      const int d = e % kD;
+      float M = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sm.m[w][g]);
+      float L = 0.0f, O = 0.0f;
+      if (M != -INFINITY) {
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+          const float mw = sm.m[w][g];
+          if (mw == -INFINITY) continue;
+          const float f = exp2f(mw - M);
+          L = fmaf(f, sm.l[w][g], L);
+          O = fmaf(f, sm.o[w][g][d], O);
+        }
+      }
+      emit(s, g, d, M, L, O);
+    }
+  }
+}
+
 __device__ __forceinline__ void write_zeros(const AttnArgs& a, int b) {
   for (int e = threadIdx.x; e < a.q_heads * kD; e += kThreads)
     a.out[int64_t(b) * a.q_heads * kD + e] = 0.0f;
@@ -323,7 +442,10 @@ __device__ __forceinline__ void write_zeros(const AttnArgs& a, int b) {
 // For each (sequence, KV head) it touches, it writes the output directly when
 // it holds all of that pair's tiles, else a partial into slot 2w (its first
 // pair) or 2w+1 (its last pair). The workgroup that holds a pair's first tile
-// records (first workgroup, last workgroup, its slot) for the combine.
+// records (first workgroup, last workgroup, its slot) for the combine. When
+// the range's segments and block ids fit in LDS (kMaxSegMax, kRangeIds), they
+// and the segments' queries are staged once and attend_range carries the
+// tile pipeline across segments; otherwise each segment runs on its own.
 template <int G, int BS, bool BF16>
 __global__ __launch_bounds__(kThreads, 2) void attn_mfma_streamk(AttnArgs a) {
   __shared__ Smem<G> sm;
@@ -381,6 +503,97 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_streamk(AttnArgs a) {
   const int per = (U + int(gridDim.x) - 1) / int(gridDim.x);
   int u = min(U, int(blockIdx.x) * per);
   const int u_end = min(U, u + per);
+
+  // The range's segments and all their block ids, staged once.
+  constexpr int kMaxSeg = max_seg<G>();
+  __shared__ SegDesc s_desc[kMaxSeg];
+  __shared__ int32_t s_rids[kRangeIds];
+  __shared__ __attribute__((aligned(16))) uint16_t s_q[kMaxSeg][G][kD];
+  int nseg = 0, nids = 0;
+  {
+    int uu = u;
+    int lo = 0, hi = B - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (s_pref[mid] <= uu) lo = mid;
+      else hi = mid - 1;
+    }
+    int b = uniform(lo);
+    while (uu < u_end && nseg <= kMaxSeg) {
+      while (uniform(s_pref[b + 1]) <= uu) ++b;
+      const int len = uniform(s_len[b]);
+      const int nt = (len + kIt - 1) / kIt;
+      const int P = nt + kSegCost;
+      const int r = uu - uniform(s_pref[b]);
+      const int kvh = r / P;
+      const int q = r - kvh * P;
+      if (q < kSegCost) {
+        uu += kSegCost - q;
+        continue;
+      }
+      const int j0 = q - kSegCost;
+      const int j1 = min(nt, j0 + (u_end - uu));
+      if (nseg < kMaxSeg && tid == 0) s_desc[nseg] = SegDesc{b, kvh, len, j0, j1, nids};
+      nids += (j1 * kIt - 1) / BS - j0 * kIt / BS + 1;
+      ++nseg;
+      uu += j1 - j0;
+    }
+  }
+  if (nseg <= kMaxSeg && nids <= kRangeIds) {
+    __syncthreads();
+    for (int e = tid; e < nids; e += kThreads) {
+      int sg = 0;
+      while (sg + 1 < nseg && s_desc[sg + 1].id0 <= e) ++sg;
+      const int b = s_desc[sg].b;
+      const int j = s_desc[sg].j0 * kIt / BS + (e - s_desc[sg].id0);
+      int id = -1;
+      if (j * BS < s_desc[sg].len) {
+        id = a.table[int64_t(b) * a.max_blocks + j];
+        if (id < 0 || id >= a.n_local) {
+          atomicAdd(a.err_count, 1);
+          id = -1;
+        }
+      }
+      s_rids[e] = id;
+    }
+    for (int e = tid; e < nseg * G * (kD / 8); e += kThreads) {   // 16-byte pieces of Q rows
+      const int s2 = e / (G * (kD / 8));
+      const int g = (e / (kD / 8)) % G;
+      const int c = e % (kD / 8);
+      const char* src = reinterpret_cast<const char*>(a.q) +
+                        ((int64_t(s_desc[s2].b) * a.q_heads + s_desc[s2].kvh * G + g) * kD + c * 8) * 2;
+      *reinterpret_cast<u32x4*>(&s_q[s2][g][c * 8]) = ld16(src);
+    }
+    __syncthreads();
+    if (tid == 0) {
+      for (int s2 = 0; s2 < nseg; ++s2) {
+        const SegDesc& d = s_desc[s2];
+        if (d.j0 != 0) continue;
+        const int nt = (d.len + kIt - 1) / kIt;
+        int32_t* info = a.info + (int64_t(d.b) * H + d.kvh) * 3;
+        info[0] = int(blockIdx.x);
+        info[1] = (s_pref[d.b] + d.kvh * (nt + kSegCost) + nt + kSegCost - 1) / per;
+        info[2] = s2 == 0 ? 0 : 1;
+      }
+    }
+    attend_range<G, BS, BF16>(a, s_desc, nseg, s_rids, s_q, sm,
+                              [&](int s2, int g, int d, float M, float L, float O) {
+      const SegDesc& sdd = s_desc[s2];
+      const int nt = (sdd.len + kIt - 1) / kIt;
+      if (sdd.j0 == 0 && sdd.j1 == nt) {
+        a.out[(int64_t(sdd.b) * a.q_heads + sdd.kvh * G + g) * kD + d] = L > 0.0f ? O / L : 0.0f;
+      } else {
+        const int64_t slot = int64_t(blockIdx.x) * 2 + (s2 == 0 ? 0 : 1);
+        a.part_o[(slot * G + g) * kD + d] = O;
+        if (d == 0) {
+          a.part_ml[(slot * G + g) * 2] = M;
+          a.part_ml[(slot * G + g) * 2 + 1] = L;
+        }
+      }
+    });
+    return;
+  }
+
   int seg = 0;
   while (u < u_end) {
     int lo = 0, hi = B - 1;   // last sequence whose first unit is <= u

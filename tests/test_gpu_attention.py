@@ -326,6 +326,21 @@ def test_llama8b_shaped_layer_sampled(ema):
         w.close()
 
 
+def test_ranges_too_long_to_stage(ema):
+    """8B-shaped heads with lengths near 8k: every stream-K range holds more
+    block ids than the kernel stages in LDS up front, so each segment takes
+    the unstaged path (sampled sequences against the oracle)."""
+    print("long ranges", flush=True)
+    cfg = synth.LLAMA8B.scaled(layers=1, lens=("uniform", 7800, 8192))
+    w = Workload(cfg, fill="device")
+    try:
+        tiles = sum((int(n) + 31) // 32 for n in w.lens) * w.hkv
+        assert tiles * 2 // 256 > 512                   # ids per range (block size 16)
+        sampled_parity(ema, w, 0, 4, np.random.default_rng(3))
+    finally:
+        w.close()
+
+
 def test_70b_tp8_share_layer_sampled(ema):
     print("70b share layer", flush=True)
     w = Workload(synth.L70B_TP8, layers=2, fill="device")
