@@ -471,8 +471,8 @@ def stress_main(args):
                       "block_sizes": list(cfg.extra["block_sizes"])},
            "roofline": {"bound": "hbm", "achieved": best, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                         "frac": best / HBM_PEAK_GBPS, "traffic": traffic,
-                        "kernel": f"block_copy_kernel (prefetch of every slice block, block "
-                                  f"size {best_bs})"},
+                        "kernel": f"block_copy_same_kernel (prefetch of every slice block, "
+                                  f"block size {best_bs})"},
            "sweep": out}
     if rec is not None:
         res["roofline"]["traffic_source"] = rec.get("note", "counter summary")

@@ -1,11 +1,16 @@
 // Block-table-driven gather/scatter of layer-blocks between the local pool and
 // the slice (prefetch before use, migration, reclaim write-back / compaction).
 //
-// Work unit: 4 KiB of one destination block, i.e. 16 tokens x 128 channels of
-// one KV head's K or V -- one block-row at block size 16. One wavefront owns a
-// unit, four per workgroup. Same-layout units are straight 16-byte-per-lane
-// copies (each wave instruction moves 1 KiB, fully coalesced). Units that
-// change layout go through the wave's LDS tile: K rows only change order
+// When both pools share one layout (the slice in the local layout), every
+// copy is a straight 16-byte-per-lane copy: one wavefront moves 2 KiB of a
+// block (two wave instructions of 1 KiB each way, fully coalesced), four
+// wavefronts per workgroup; measured against 1, 4 and 8 KiB per wavefront,
+// 2 KiB moves the most bytes per second.
+//
+// Otherwise the work unit is 4 KiB of one destination block, i.e. 16 tokens x
+// 128 channels of one KV head's K or V -- one block-row at block size 16. One
+// wavefront owns a unit, four per workgroup. Same-layout units are straight
+// copies as above. Units that change layout go through the wave's LDS tile: K rows only change order
 // (256-byte rows are re-addressed, no LDS), V is transposed between
 // [token][channel] (NHD) and [channel][token] (ATTN) in LDS so that both the
 // global reads and the global writes stay 16 bytes per lane. Into ATTN, a V
@@ -22,7 +27,8 @@ namespace {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kUnitBytes = 4096;
+constexpr int kUnitBytes = 4096;    // work unit of the layout-changing kernel
+constexpr int kPieceBytes = 2048;   // work unit of the same-layout kernel
 constexpr int kWaves = 4;
 constexpr int kTileRow = 128 + 8;   // u16 per LDS tile row (padded, keeps 16 B alignment)
 
@@ -188,6 +194,38 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
 // One workgroup per (sequence, KV head), one thread per channel: the K element
 // goes to the token's row, the V element to the token's column of the
 // transposed V rows.
+// Same-layout copy (both pools in the local layout): wave w of workgroup g
+// moves piece g*kWaves + w, 2 KiB of block src_ids[i] to the same offset of
+// block dst_ids[i]. Out-of-range ids are skipped and counted once per block.
+__global__ __launch_bounds__(256) void block_copy_same_kernel(PoolView pv,
+                                                              const int32_t* __restrict__ src_ids,
+                                                              const int32_t* __restrict__ dst_ids,
+                                                              int32_t n, int32_t* err_count) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int ppb = int(pv.block_bytes / kPieceBytes);
+  const int64_t piece = int64_t(blockIdx.x) * kWaves + wave;
+  if (piece >= int64_t(n) * ppb) return;
+  const int32_t i = int32_t(piece / ppb);
+  const int k = int(piece - int64_t(i) * ppb);
+  const int32_t s = src_ids[i];
+  const int32_t d = dst_ids[i];
+  const int32_t n_total = pv.n_local + pv.n_slice;
+  if (s < 0 || s >= n_total || d < 0 || d >= n_total) {
+    if (k == 0 && lane == 0) atomicAdd(err_count, 1);
+    return;
+  }
+  const char* sb = s < pv.n_local ? pv.local + int64_t(s) * pv.block_bytes
+                                  : pv.slice + int64_t(s - pv.n_local) * pv.block_bytes;
+  char* db = d < pv.n_local ? pv.local + int64_t(d) * pv.block_bytes
+                            : pv.slice + int64_t(d - pv.n_local) * pv.block_bytes;
+  const int64_t off = int64_t(k) * kPieceBytes + lane * 16;
+  const u32x4 v0 = ld16(sb + off);
+  const u32x4 v1 = ld16(sb + off + 1024);
+  st16(db + off, v0);
+  st16(db + off + 1024, v1);
+}
+
 __global__ __launch_bounds__(128) void kv_append_kernel(PoolView pv, const uint16_t* __restrict__ k_new,
                                                         const uint16_t* __restrict__ v_new,
                                                         const int32_t* __restrict__ table,
@@ -245,15 +283,20 @@ __global__ void table_rewrite_kernel(int32_t* __restrict__ tables, int64_t n_ent
 hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32_t* dst,
                              int32_t n, int32_t* err_count, hipStream_t stream) {
   if (n <= 0) return hipSuccess;
-  const int64_t upb = pv.block_bytes / kUnitBytes;
-  const size_t lds = pv.slice_layout == 0 ? 0 : size_t(kWaves) * tile_elems(pv.block_size) * 2;
+  const bool same = pv.slice_layout == 0;
+  const int64_t upb = pv.block_bytes / (same ? kPieceBytes : kUnitBytes);   // waves per block
+  const size_t lds = same ? 0 : size_t(kWaves) * tile_elems(pv.block_size) * 2;
   // A launch stays below 2^32 work-items: at most 2^24 workgroups of 256.
   const int64_t max_blocks = std::max<int64_t>(1, (int64_t(1) << 24) * kWaves / upb);
   for (int64_t b0 = 0; b0 < n; b0 += max_blocks) {
     const int32_t m = int32_t(std::min<int64_t>(max_blocks, n - b0));
     const int64_t grid = (int64_t(m) * upb + kWaves - 1) / kWaves;
-    hipLaunchKernelGGL(block_copy_kernel, dim3(unsigned(grid)), dim3(256), lds, stream, pv,
-                       src + b0, dst + b0, m, err_count);
+    if (same)
+      hipLaunchKernelGGL(block_copy_same_kernel, dim3(unsigned(grid)), dim3(256), 0, stream, pv,
+                         src + b0, dst + b0, m, err_count);
+    else
+      hipLaunchKernelGGL(block_copy_kernel, dim3(unsigned(grid)), dim3(256), lds, stream, pv,
+                         src + b0, dst + b0, m, err_count);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
