@@ -2,10 +2,13 @@
 // the slice (prefetch before use, migration, reclaim write-back / compaction).
 //
 // When both pools share one layout (the slice in the local layout), every
-// copy is a straight 16-byte-per-lane copy: one wavefront moves 2 KiB of a
-// block (two wave instructions of 1 KiB each way, fully coalesced), four
-// wavefronts per workgroup; measured against 1, 4 and 8 KiB per wavefront,
-// 2 KiB moves the most bytes per second.
+// copy is a straight 16-byte-per-lane copy: a wavefront moves 2 KiB of a
+// block (two wave instructions of 1 KiB each way, fully coalesced; 1, 4, 8
+// and 16 KiB per wavefront move fewer bytes per second). Lists of up to 2^22
+// pieces (8 GiB) of scattered blocks of up to 64 KiB go one wavefront per
+// workgroup, which spreads each block over all XCDs; long ascending runs,
+// larger blocks and larger lists go four wavefronts (8 KiB contiguous) per
+// workgroup, which measured faster or steadier for them.
 //
 // Otherwise the work unit is 4 KiB of one destination block, i.e. 16 tokens x
 // 128 channels of one KV head's K or V -- one block-row at block size 16. One
@@ -195,16 +198,16 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
 // goes to the token's row, the V element to the token's column of the
 // transposed V rows.
 // Same-layout copy (both pools in the local layout): wave w of workgroup g
-// moves piece g*kWaves + w, 2 KiB of block src_ids[i] to the same offset of
-// block dst_ids[i]. Out-of-range ids are skipped and counted once per block.
+// (blockDim.x / 64 waves each) moves piece g * (blockDim.x / 64) + w, 2 KiB of
+// block src_ids[i] to the same offset of block dst_ids[i]. Out-of-range ids
+// are skipped and counted once per block.
 __global__ __launch_bounds__(256) void block_copy_same_kernel(PoolView pv,
                                                               const int32_t* __restrict__ src_ids,
                                                               const int32_t* __restrict__ dst_ids,
                                                               int32_t n, int32_t* err_count) {
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
   const int ppb = int(pv.block_bytes / kPieceBytes);
-  const int64_t piece = int64_t(blockIdx.x) * kWaves + wave;
+  const int64_t piece = int64_t(blockIdx.x) * (blockDim.x >> 6) + (threadIdx.x >> 6);
   if (piece >= int64_t(n) * ppb) return;
   const int32_t i = int32_t(piece / ppb);
   const int k = int(piece - int64_t(i) * ppb);
@@ -281,19 +284,22 @@ __global__ void table_rewrite_kernel(int32_t* __restrict__ tables, int64_t n_ent
 }  // namespace
 
 hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32_t* dst,
-                             int32_t n, int32_t* err_count, hipStream_t stream) {
+                             int32_t n, int32_t* err_count, hipStream_t stream, bool runs) {
   if (n <= 0) return hipSuccess;
   const bool same = pv.slice_layout == 0;
   const int64_t upb = pv.block_bytes / (same ? kPieceBytes : kUnitBytes);   // waves per block
+  const int wg_waves =
+      same && !runs && pv.block_bytes <= 65536 && int64_t(n) * upb <= (int64_t(1) << 22) ? 1
+                                                                                        : kWaves;
   const size_t lds = same ? 0 : size_t(kWaves) * tile_elems(pv.block_size) * 2;
-  // A launch stays below 2^32 work-items: at most 2^24 workgroups of 256.
-  const int64_t max_blocks = std::max<int64_t>(1, (int64_t(1) << 24) * kWaves / upb);
+  // A launch stays below 2^32 work-items: at most 2^25 wavefronts.
+  const int64_t max_blocks = std::max<int64_t>(1, (int64_t(1) << 25) / upb);
   for (int64_t b0 = 0; b0 < n; b0 += max_blocks) {
     const int32_t m = int32_t(std::min<int64_t>(max_blocks, n - b0));
-    const int64_t grid = (int64_t(m) * upb + kWaves - 1) / kWaves;
+    const int64_t grid = (int64_t(m) * upb + wg_waves - 1) / wg_waves;
     if (same)
-      hipLaunchKernelGGL(block_copy_same_kernel, dim3(unsigned(grid)), dim3(256), 0, stream, pv,
-                         src + b0, dst + b0, m, err_count);
+      hipLaunchKernelGGL(block_copy_same_kernel, dim3(unsigned(grid)), dim3(64 * wg_waves), 0,
+                         stream, pv, src + b0, dst + b0, m, err_count);
     else
       hipLaunchKernelGGL(block_copy_kernel, dim3(unsigned(grid)), dim3(256), lds, stream, pv,
                          src + b0, dst + b0, m, err_count);

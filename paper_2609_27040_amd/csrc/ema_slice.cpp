@@ -415,7 +415,7 @@ int ema_slice_prefetch_runs(ema_slice_t h, const int32_t* src_first, const int32
           "hipMemcpyAsync(runs)");
   HIP_TRY(hipEventRecord(h->h_work_ev, st), "hipEventRecord(runs)");
   h->h_work_pending = true;
-  HIP_TRY(ema::launch_block_copy(pool_view(h), h->d_work, h->d_work + n, n, h->d_err, st),
+  HIP_TRY(ema::launch_block_copy(pool_view(h), h->d_work, h->d_work + n, n, h->d_err, st, true),
           "prefetch_runs launch");
   return EMA_OK;
 } catch (...) {
@@ -535,7 +535,7 @@ int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, in
   const int32_t* dvals = h->d_work + np;
   const ema::PoolView pv = pool_view(h);
   const int32_t n_total = pv.n_local + pv.n_slice;
-  HIP_TRY(ema::launch_block_copy(pv, dkeys, dvals, m, h->d_err, st), "reclaim copy");
+  HIP_TRY(ema::launch_block_copy(pv, dkeys, dvals, m, h->d_err, st, true), "reclaim copy");
   if (rewrite) {
     HIP_TRY(ema::launch_remap_scatter(h->d_remap, n_total, dkeys, dvals, np, st), "remap set");
     HIP_TRY(ema::launch_table_rewrite(canon_tables, n_entries, h->d_remap, n_total, st),

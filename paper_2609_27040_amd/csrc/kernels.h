@@ -21,8 +21,12 @@ struct PoolView {
 
 // dst[i] <- src[i] for i < n (unified ids), re-laid between pool layouts.
 // Ids outside [0, n_local + n_slice) are skipped and counted in *err_count.
+// `runs`: the lists are mostly ascending runs of ids (reclaim moves,
+// contiguous-run prefetches) rather than scattered blocks; only the work
+// distribution depends on it.
 hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32_t* dst,
-                             int32_t n, int32_t* err_count, hipStream_t stream);
+                             int32_t n, int32_t* err_count, hipStream_t stream,
+                             bool runs = false);
 
 // New decode token of every sequence into its block (ATTN layout): row
 // (len-1) % bs of local block table[b][(len-1) / bs], len = seq_lens[b] > 0.
