@@ -67,7 +67,7 @@ struct AttnArgs {
 
 constexpr int kAttnChunk = 256;        // tokens per workgroup of the vector-ALU kernel
 constexpr int kMfmaGridChunk = 1024;   // tokens per workgroup of the matrix-core grid form
-constexpr int kStreamKMaxBatch = 2048; // sequences the stream-K work list holds
+constexpr int kStreamKMaxBatch = 4096; // sequences the stream-K work list holds (32 KiB of LDS)
 constexpr int kMaxStreamGrid = 2048;   // stream-K workgroups (partial slots: 2 each)
 
 // Vector-ALU kernel (v_dot2 scores, FMA outputs) plus a separate split-K merge.

@@ -51,7 +51,7 @@ constexpr int kThreads = kWaves * 64;
 constexpr int kIt = 32;                    // tokens per tile (one wave iteration)
 constexpr int kPieceTiles = 32;            // tiles whose block ids are staged in LDS at once
 constexpr int kMaxIds = kPieceTiles * kIt / 16;
-constexpr int kMaxPersistBatch = 2048;     // sequences the stream-K work list holds in LDS
+constexpr int kMaxPersistBatch = kStreamKMaxBatch;   // sequences the stream-K work list holds in LDS
 constexpr int kGridChunkTiles = 32;        // tiles per workgroup in the grid fallback
 // Each (sequence, KV head) a workgroup touches costs it several tiles' time
 // (the four wavefronts merge and a partial is written; without the staged

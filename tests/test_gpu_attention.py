@@ -186,10 +186,12 @@ def test_wide_batch_takes_the_long_chunk_path(ema, impl):
         w.close()
 
 
-@pytest.mark.parametrize("batch,hi,hkv,hq", [(600, 100, 2, 8), (2100, 40, 1, 4)])
+@pytest.mark.parametrize("batch,hi,hkv,hq", [(600, 100, 2, 8), (2100, 40, 1, 4),
+                                             (8192, 24, 1, 4), (8300, 16, 1, 2)])
 def test_many_short_sequences(ema, impl, batch, hi, hkv, hq):
     """Stream-K ranges then cover several whole sequences each (written
-    directly) plus cut ones; above 2048 sequences the grid form takes over."""
+    directly) plus cut ones, and more segments than a range stages up front;
+    above 4096 sequences the grid form takes over."""
     print(f"short {impl} batch={batch}", flush=True)
     rng = np.random.default_rng(batch)
     lens = rng.integers(0, hi + 1, batch).tolist()
