@@ -589,7 +589,7 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
   // list, else a grid of 1024-token chunks. Vector-ALU kernel: a grid of
   // 256-token chunks. Grid forms keep one partial per (sequence, head, chunk).
   const int64_t tiles = int64_t(batch) * hkv * ((max_tokens + 31) / 32);
-  const bool stream_k = !h->attn_valu && !h->attn_grid && batch <= ema::kStreamKMaxBatch &&
+  const bool stream_k = !h->attn_valu && !h->attn_grid && batch <= ema::streamk_max_batch(G) &&
                         tiles < (int64_t(1) << 30);
   const int32_t chunk = h->attn_valu ? ema::kAttnChunk : ema::kMfmaGridChunk;
   const int32_t n_split = int32_t(std::max<int64_t>(1, (max_tokens + chunk - 1) / chunk));

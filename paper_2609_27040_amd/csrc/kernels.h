@@ -67,7 +67,11 @@ struct AttnArgs {
 
 constexpr int kAttnChunk = 256;        // tokens per workgroup of the vector-ALU kernel
 constexpr int kMfmaGridChunk = 1024;   // tokens per workgroup of the matrix-core grid form
-constexpr int kStreamKMaxBatch = 4096; // sequences the stream-K work list holds (32 KiB of LDS)
+// Sequences the stream-K work list holds in LDS (lengths and prefix sums):
+// sized so that a workgroup's LDS stays within half a CU's 160 KiB, which
+// every call measured faster (16 query heads per KV head need twice the
+// merge space, hence the smaller list).
+constexpr int streamk_max_batch(int group) { return group >= 16 ? 2048 : 4096; }
 constexpr int kMaxStreamGrid = 2048;   // stream-K workgroups (partial slots: 2 each)
 
 // Vector-ALU kernel (v_dot2 scores, FMA outputs) plus a separate split-K merge.

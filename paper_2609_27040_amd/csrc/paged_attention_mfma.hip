@@ -51,7 +51,6 @@ constexpr int kThreads = kWaves * 64;
 constexpr int kIt = 32;                    // tokens per tile (one wave iteration)
 constexpr int kPieceTiles = 32;            // tiles whose block ids are staged in LDS at once
 constexpr int kMaxIds = kPieceTiles * kIt / 16;
-constexpr int kMaxPersistBatch = kStreamKMaxBatch;   // sequences the stream-K work list holds in LDS
 constexpr int kGridChunkTiles = 32;        // tiles per workgroup in the grid fallback
 // Each (sequence, KV head) a workgroup touches costs it several tiles' time
 // (the four wavefronts merge and a partial is written; without the staged
@@ -449,8 +448,8 @@ __device__ __forceinline__ void write_zeros(const AttnArgs& a, int b) {
 template <int G, int BS, bool BF16>
 __global__ __launch_bounds__(kThreads, 2) void attn_mfma_streamk(AttnArgs a) {
   __shared__ Smem<G> sm;
-  __shared__ int32_t s_len[kMaxPersistBatch];
-  __shared__ int32_t s_pref[kMaxPersistBatch + 1];
+  __shared__ int32_t s_len[streamk_max_batch(G)];
+  __shared__ int32_t s_pref[streamk_max_batch(G) + 1];
   __shared__ int32_t s_seg[kThreads];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
