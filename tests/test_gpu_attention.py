@@ -187,11 +187,13 @@ def test_wide_batch_takes_the_long_chunk_path(ema, impl):
 
 
 @pytest.mark.parametrize("batch,hi,hkv,hq", [(600, 100, 2, 8), (2100, 40, 1, 4),
-                                             (8192, 24, 1, 4), (8300, 16, 1, 2)])
+                                             (4096, 24, 1, 4), (4200, 16, 1, 2),
+                                             (2048, 20, 1, 16), (2100, 20, 1, 16)])
 def test_many_short_sequences(ema, impl, batch, hi, hkv, hq):
     """Stream-K ranges then cover several whole sequences each (written
     directly) plus cut ones, and more segments than a range stages up front;
-    above 4096 sequences the grid form takes over."""
+    above 4096 sequences (2048 with 16 query heads per KV head) the grid form
+    takes over."""
     print(f"short {impl} batch={batch}", flush=True)
     rng = np.random.default_rng(batch)
     lens = rng.integers(0, hi + 1, batch).tolist()
