@@ -212,6 +212,30 @@ def cpu_baseline(w, seconds):
             "host_cores_available": len(os.sched_getaffinity(0))}
 
 
+def cpu_copy_baseline(rows, layout, hkv, D, bs, seconds):
+    """The oracle's block copy (slice layout -> local layout) on this host,
+    one thread, over host copies of sampled slice blocks (rows: uint8
+    [n][block bytes]) for about `seconds`; GB/s of read + write."""
+    import oracle
+    from threadpoolctl import threadpool_limits
+
+    dst = np.empty_like(rows)
+    n_cp = 0
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < seconds:
+            i = n_cp % len(rows)
+            dst[i] = oracle.convert_block(rows[i], layout, oracle.LAYOUT_ATTN, hkv, D, bs)
+            n_cp += 1
+        t = time.perf_counter() - t0
+    return {"value": 2 * n_cp * rows.shape[1] / t / 1e9, "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": (f"{n_cp} single-block copies of {rows.shape[1] >> 10} KiB by the oracle "
+                       f"({t:.1f} s, one thread), cycling over {len(rows)} slice blocks read "
+                       f"back from the device"),
+            "host_cores_available": len(os.sched_getaffinity(0))}
+
+
 def symmetry(w, out, s, reps, ema, torch):
     """Staged versus all-local attention tables over the same tokens.
 
@@ -438,11 +462,18 @@ def stress_main(args):
     torch.cuda.set_device(0)
     cfg = synth.STRESS
     out = {}
+    cpu = None
     for bs in cfg.extra["block_sizes"]:
         log(f"stress block size {bs}: {stress_blocks(cfg, bs)} blocks")
         run = StressRun(bs)
         try:
             pf = run.prefetch_all()
+            if cpu is None and not args.no_cpu_baseline:
+                log("cpu baseline (oracle block copies)")
+                ids = run.w.pf_src[0][run._sample(len(run.w.pf_src[0]))]
+                cpu = cpu_copy_baseline(run._rows(ids), run.layout, run.w.hkv, run.w.D, bs,
+                                        args.cpu_seconds / 2)
+                cpu["block_size"] = bs
             run.free_staging()
             rc = run.reclaim_sweep()
         finally:
@@ -476,6 +507,8 @@ def stress_main(args):
            "sweep": out}
     if rec is not None:
         res["roofline"]["traffic_source"] = rec.get("note", "counter summary")
+    if cpu is not None:
+        res["cpu_baseline"] = cpu
     print(json.dumps(res))
 
 
