@@ -55,10 +55,13 @@ constexpr int kGridChunkTiles = 32;        // tiles per workgroup in the grid fa
 // Each (sequence, KV head) a workgroup touches costs it several tiles' time
 // (the four wavefronts merge and a partial is written; without the staged
 // range below, the tile pipeline also drains and refills); the stream-K split
-// counts it as kSegCost tiles so that workgroups that touch more pairs get
-// fewer tiles (measured best between 6 and 10 on 32-token tiles with one
-// workgroup per CU).
-constexpr int kSegCost = 8;
+// counts it as seg_cost<G>() tiles so that workgroups that touch more pairs
+// get fewer tiles. Measured on 32-token tiles with one workgroup per CU: 8 is
+// best between 6 and 10 at 4 and 8 query heads per KV head; 16 query heads,
+// whose merge and partials are four times larger, do best with 16 (against
+// 8, 12 and 24).
+template <int G>
+constexpr int seg_cost() { return G >= 16 ? 16 : 8; }
 // A stream-K range whose segments and block ids fit these bounds is staged
 // in LDS up front, so each segment can start while the previous one merges.
 constexpr int kMaxSegMax = 8;              // segments of a range (4 for G = 16)
@@ -435,9 +438,10 @@ __device__ __forceinline__ void write_zeros(const AttnArgs& a, int b) {
 }
 
 // Stream-K form. Every workgroup reads all lengths once and prefix-sums the
-// unit counts (n_t(b) + kSegCost) * Hkv in LDS; units are ordered (sequence,
-// KV head, unit), each pair's kSegCost cost units (no tiles) ahead of its n_t
-// tiles, and workgroup w takes units [w*per, (w+1)*per), per = ceil(U/grid).
+// unit counts (n_t(b) + kSegCost) * Hkv in LDS (kSegCost = seg_cost<G>());
+// units are ordered (sequence, KV head, unit), each pair's kSegCost cost
+// units (no tiles) ahead of its n_t tiles, and workgroup w takes units
+// [w*per, (w+1)*per), per = ceil(U/grid).
 // For each (sequence, KV head) it touches, it writes the output directly when
 // it holds all of that pair's tiles, else a partial into slot 2w (its first
 // pair) or 2w+1 (its last pair). The workgroup that holds a pair's first tile
@@ -447,6 +451,7 @@ __device__ __forceinline__ void write_zeros(const AttnArgs& a, int b) {
 // tile pipeline across segments; otherwise each segment runs on its own.
 template <int G, int BS, bool BF16>
 __global__ __launch_bounds__(kThreads, 2) void attn_mfma_streamk(AttnArgs a) {
+  constexpr int kSegCost = seg_cost<G>();
   __shared__ Smem<G> sm;
   __shared__ int32_t s_len[streamk_max_batch(G)];
   __shared__ int32_t s_pref[streamk_max_batch(G) + 1];
