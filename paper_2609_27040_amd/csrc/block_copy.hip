@@ -13,14 +13,16 @@
 // Otherwise the work unit is 4 KiB of one destination block, i.e. 16 tokens x
 // 128 channels of one KV head's K or V -- one block-row at block size 16. One
 // wavefront owns a unit, four per workgroup. Same-layout units are straight
-// copies as above. Units that change layout go through the wave's LDS tile: K rows only change order
-// (256-byte rows are re-addressed, no LDS), V is transposed between
-// [token][channel] (NHD) and [channel][token] (ATTN) in LDS so that both the
-// global reads and the global writes stay 16 bytes per lane. Into ATTN, a V
-// unit is all BS tokens of 2048/BS channels, so every transposed row it writes
-// is whole; out of ATTN it is 16 tokens of all 128 channels, so every token
-// row it writes is whole. The tile is dynamic LDS, requested only when the
-// slice layout differs from the local one.
+// copies as above. Units that change layout go through the wave's LDS tile:
+// K rows only change order (256-byte rows are re-addressed, no LDS), V is
+// transposed between [token][channel] (NHD) and [channel][token] (ATTN) in
+// LDS so that both the global reads and the global writes stay 16 bytes per
+// lane. Into ATTN, a V unit is T = min(BS, 64) tokens of 2048/T channels: its
+// transposed rows are written whole up to 64 tokens (128 B), its token rows
+// are read 64 B or more at a time, and the four units of a workgroup cover
+// whole 256-B token rows; out of ATTN it is 16 tokens of all 128 channels, so
+// every token row it writes is whole. The tile is dynamic LDS, requested only
+// when the slice layout differs from the local one.
 #include "kernels.h"
 
 #include <algorithm>
@@ -35,10 +37,16 @@ constexpr int kPieceBytes = 2048;   // work unit of the same-layout kernel
 constexpr int kWaves = 4;
 constexpr int kTileRow = 128 + 8;   // u16 per LDS tile row (padded, keeps 16 B alignment)
 
+// Tokens of one V unit into the local layout: whole transposed rows up to 64
+// tokens (128 B); with larger blocks a unit is 64 tokens x 32 channels, and
+// the four units of a workgroup cover one token group's 128 channels.
+__host__ __device__ constexpr int v_unit_tokens(int bs) { return bs < 64 ? bs : 64; }
+
 // u16 per wave of the relayout tile: 16 x kTileRow (out of ATTN) or
-// BS x (2048/BS + 8) (into ATTN).
+// T x (2048/T + 8), T = v_unit_tokens(bs) (into ATTN).
 __host__ __device__ constexpr int tile_elems(int bs) {
-  return 16 * kTileRow > 2048 + 8 * bs ? 16 * kTileRow : 2048 + 8 * bs;
+  return 16 * kTileRow > 2048 + 8 * v_unit_tokens(bs) ? 16 * kTileRow
+                                                      : 2048 + 8 * v_unit_tokens(bs);
 }
 
 // Block data is touched once per copy: streaming (non-temporal) loads and
@@ -98,7 +106,8 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
   }
 
   // Layout change. Unit k -> (half, head h, group tg): a 16-token group, or
-  // for V into ATTN a group of 2048/BS channels (BS/16 groups either way).
+  // for V into ATTN a group of T tokens x 2048/T channels (BS/16 groups
+  // either way).
   const int H = pv.kv_heads;
   const int BS = pv.block_size;
   const int tgs = BS / 16;
@@ -131,23 +140,28 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
   const char* sv = sb + half_bytes;
   char* dv = db + half_bytes;
   if (s_nhd) {
-    // NHD -> ATTN, unit (h, channel group tg): all BS tokens of C = 2048/BS
-    // channels. Read C channels of every token row (LR lanes per row) into the
-    // tile as [t][c], then write C whole transposed rows of BS tokens (LC lanes
-    // each).
-    const int C = 2048 / BS;
-    const int c0 = tg * C;
+    // NHD -> ATTN, unit (h, token group, channel group): T = v_unit_tokens(BS)
+    // tokens of C = 2048/T channels. Read C channels of each of the T token
+    // rows (LR lanes per row) into the tile as [t][c], then write C
+    // transposed rows of T tokens (LC lanes each): reads and writes stay at
+    // least 64 B contiguous, and the four waves of a workgroup read whole
+    // 256-B token rows between them.
+    const int T = v_unit_tokens(BS);
+    const int C = 2048 / T;
+    const int cgs = 128 / C;                  // channel groups per token group
+    const int t_base = (tg / cgs) * T;
+    const int c0 = (tg % cgs) * C;
     const int LR = C / 8;
     const int stride = C + 8;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int t = j * (64 / LR) + lane / LR;
       const int c = (lane % LR) * 8;
-      const u32x4 v = ld16(sv + (int64_t(t * H + h) * 128 + c0 + c) * 2);
+      const u32x4 v = ld16(sv + (int64_t((t_base + t) * H + h) * 128 + c0 + c) * 2);
       *reinterpret_cast<u32x4*>(&tw[t * stride + c]) = v;
     }
     wave_lds_sync();
-    const int LC = BS / 8;
+    const int LC = T / 8;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int item = j * 64 + lane;
@@ -159,7 +173,7 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
         w[q] = uint32_t(tw[(t0 + 2 * q) * stride + cc]) |
                (uint32_t(tw[(t0 + 2 * q + 1) * stride + cc]) << 16);
       const u32x4 out = {w[0], w[1], w[2], w[3]};
-      st16(dv + (int64_t(h * 128 + c0 + cc) * BS + t0) * 2, out);
+      st16(dv + (int64_t(h * 128 + c0 + cc) * BS + t_base + t0) * 2, out);
     }
   } else {
     // ATTN -> NHD. Read 128 channel rows x 16 tokens, scatter into the tile as

@@ -98,7 +98,7 @@ def assert_pools_equal(gpu, st):
 
 @pytest.mark.parametrize("layout", [0, 1])
 @pytest.mark.parametrize("bs,hkv,dtype", [(16, 2, "f16"), (32, 1, "bf16"), (64, 8, "bf16"),
-                                          (256, 2, "f16"), (16, 8, "bf16")])
+                                          (128, 4, "bf16"), (256, 2, "f16"), (16, 8, "bf16")])
 def test_prefetch_matches_oracle_bit_for_bit(ema, layout, bs, hkv, dtype):
     print(f"prefetch layout={layout} bs={bs} hkv={hkv} {dtype}", flush=True)
     n_local, n_slice = 40, 30
