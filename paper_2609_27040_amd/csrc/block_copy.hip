@@ -20,8 +20,9 @@
 // lane. Into ATTN, a V unit is T = min(BS, 64) tokens of 2048/T channels: its
 // transposed rows are written whole up to 64 tokens (128 B), its token rows
 // are read 64 B or more at a time, and the four units of a workgroup cover
-// whole 256-B token rows; out of ATTN it is 16 tokens of all 128 channels, so
-// every token row it writes is whole. The tile is dynamic LDS, requested only
+// whole 256-B token rows; out of ATTN it is 16 tokens of all 128 channels
+// (whole token rows written), or from block size 64 on 64 tokens of 32
+// channels (128-B channel rows read). The tile is dynamic LDS, requested only
 // when the slice layout differs from the local one.
 #include "kernels.h"
 
@@ -42,7 +43,7 @@ constexpr int kTileRow = 128 + 8;   // u16 per LDS tile row (padded, keeps 16 B 
 // the four units of a workgroup cover one token group's 128 channels.
 __host__ __device__ constexpr int v_unit_tokens(int bs) { return bs < 64 ? bs : 64; }
 
-// u16 per wave of the relayout tile: 16 x kTileRow (out of ATTN) or
+// u16 per wave of the relayout tile: 16 x kTileRow or 64 x 40 (out of ATTN),
 // T x (2048/T + 8), T = v_unit_tokens(bs) (into ATTN).
 __host__ __device__ constexpr int tile_elems(int bs) {
   return 16 * kTileRow > 2048 + 8 * v_unit_tokens(bs) ? 16 * kTileRow
@@ -176,34 +177,48 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
       st16(dv + (int64_t(h * 128 + c0 + cc) * BS + t_base + t0) * 2, out);
     }
   } else {
-    // ATTN -> NHD. Read 128 channel rows x 16 tokens, scatter into the tile as
-    // [t][c], then write 16 whole token rows.
+    // ATTN -> NHD, unit (h, token group, channel group): T = 16 tokens of all
+    // 128 channels, or from block size 64 on T = 64 tokens of 32 channels.
+    // Read the unit's C channel rows of T tokens (T/8 lanes per row), scatter
+    // into the tile as [t][c], then write T token rows of C channels (C/8
+    // lanes per row): whole 256-B token rows at T = 16; at T = 64, 128-B
+    // channel-row reads, 64-B token-row writes, and the four units of a
+    // workgroup write whole token rows between them.
+    const int T = BS >= 64 ? 64 : 16;
+    const int C = 2048 / T;
+    const int cgs = 128 / C;
+    const int t_base = (tg / cgs) * T;
+    const int c0 = (tg % cgs) * C;
+    const int IR = T / 8;                     // 16-B items per channel row
+    const int stride = C + 8;
     u32x4 v[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int item = j * 64 + lane;
-      const int c = item >> 1;
-      const int t0 = (item & 1) * 8;
-      v[j] = ld16(sv + (int64_t(h * 128 + c) * BS + tg * 16 + t0) * 2);
+      const int c = item / IR;
+      const int t0 = (item % IR) * 8;
+      v[j] = ld16(sv + (int64_t(h * 128 + c0 + c) * BS + t_base + t0) * 2);
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int item = j * 64 + lane;
-      const int c = item >> 1;
-      const int t0 = (item & 1) * 8;
+      const int c = item / IR;
+      const int t0 = (item % IR) * 8;
       const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        tw[(t0 + 2 * q) * kTileRow + c] = uint16_t(w[q] & 0xffffu);
-        tw[(t0 + 2 * q + 1) * kTileRow + c] = uint16_t(w[q] >> 16);
+        tw[(t0 + 2 * q) * stride + c] = uint16_t(w[q] & 0xffffu);
+        tw[(t0 + 2 * q + 1) * stride + c] = uint16_t(w[q] >> 16);
       }
     }
     wave_lds_sync();
+    const int LW = C / 8;                     // lanes per token row written
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int tl = j * 4 + (lane >> 4);
-      const u32x4 out = *reinterpret_cast<const u32x4*>(&tw[tl * kTileRow + (lane & 15) * 8]);
-      st16(dv + int64_t((tg * 16 + tl) * H + h) * 256 + (lane & 15) * 16, out);
+      const int tl = j * (64 / LW) + lane / LW;
+      const int cp = (lane % LW) * 8;
+      const u32x4 out = *reinterpret_cast<const u32x4*>(&tw[tl * stride + cp]);
+      st16(dv + (int64_t((t_base + tl) * H + h) * 128 + c0 + cp) * 2, out);
     }
   }
 }
