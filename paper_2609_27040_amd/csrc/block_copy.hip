@@ -21,8 +21,8 @@
 // transposed rows are written whole up to 64 tokens (128 B), its token rows
 // are read 64 B or more at a time, and the four units of a workgroup cover
 // whole 256-B token rows; out of ATTN it is 16 tokens of all 128 channels
-// (whole token rows written), or from block size 64 on 64 tokens of 32
-// channels (128-B channel rows read). The tile is dynamic LDS, requested only
+// (whole token rows written), or from block size 64 on 32 tokens of 64
+// channels (128-B pieces of token rows written). The tile is dynamic LDS, requested only
 // when the slice layout differs from the local one.
 #include "kernels.h"
 
@@ -43,7 +43,7 @@ constexpr int kTileRow = 128 + 8;   // u16 per LDS tile row (padded, keeps 16 B 
 // the four units of a workgroup cover one token group's 128 channels.
 __host__ __device__ constexpr int v_unit_tokens(int bs) { return bs < 64 ? bs : 64; }
 
-// u16 per wave of the relayout tile: 16 x kTileRow or 64 x 40 (out of ATTN),
+// u16 per wave of the relayout tile: 16 x kTileRow or 32 x 72 (out of ATTN),
 // T x (2048/T + 8), T = v_unit_tokens(bs) (into ATTN).
 __host__ __device__ constexpr int tile_elems(int bs) {
   return 16 * kTileRow > 2048 + 8 * v_unit_tokens(bs) ? 16 * kTileRow
@@ -178,13 +178,13 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
     }
   } else {
     // ATTN -> NHD, unit (h, token group, channel group): T = 16 tokens of all
-    // 128 channels, or from block size 64 on T = 64 tokens of 32 channels.
+    // 128 channels, or from block size 64 on T = 32 tokens of 64 channels.
     // Read the unit's C channel rows of T tokens (T/8 lanes per row), scatter
     // into the tile as [t][c], then write T token rows of C channels (C/8
-    // lanes per row): whole 256-B token rows at T = 16; at T = 64, 128-B
-    // channel-row reads, 64-B token-row writes, and the four units of a
-    // workgroup write whole token rows between them.
-    const int T = BS >= 64 ? 64 : 16;
+    // lanes per row): whole 256-B token rows at T = 16; at T = 32, 64-B
+    // channel-row reads and 128-B token-row writes (measured faster than
+    // 64 tokens of 32 channels, whose writes are 64 B).
+    const int T = BS >= 64 ? 32 : 16;
     const int C = 2048 / T;
     const int cgs = 128 / C;
     const int t_base = (tg / cgs) * T;
