@@ -223,9 +223,6 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
   }
 }
 
-// One workgroup per (sequence, KV head), one thread per channel: the K element
-// goes to the token's row, the V element to the token's column of the
-// transposed V rows.
 // Same-layout copy (both pools in the local layout): wave w of workgroup g
 // (blockDim.x / 64 waves each) moves piece g * (blockDim.x / 64) + w, 2 KiB of
 // block src_ids[i] to the same offset of block dst_ids[i]. Out-of-range ids
@@ -258,6 +255,9 @@ __global__ __launch_bounds__(256) void block_copy_same_kernel(PoolView pv,
   st16(db + off + 1024, v1);
 }
 
+// One workgroup per (sequence, KV head), one thread per channel: the K element
+// goes to the token's row, the V element to the token's column of the
+// transposed V rows.
 __global__ __launch_bounds__(128) void kv_append_kernel(PoolView pv, const uint16_t* __restrict__ k_new,
                                                         const uint16_t* __restrict__ v_new,
                                                         const int32_t* __restrict__ table,
