@@ -450,6 +450,10 @@ __device__ __forceinline__ void write_zeros(const AttnArgs& a, int b) {
 // and the segments' queries are staged once and attend_range carries the
 // tile pipeline across segments; otherwise each segment runs on its own.
 template <int G, int BS, bool BF16>
+// Compiled as if two workgroups shared a CU (at most 256 registers a lane),
+// although one per CU is launched: under the looser bound the compiler's
+// schedule (which then also used accumulation registers) ran every call
+// 11-12 % slower.
 __global__ __launch_bounds__(kThreads, 2) void attn_mfma_streamk(AttnArgs a) {
   constexpr int kSegCost = seg_cost<G>();
   __shared__ Smem<G> sm;
