@@ -22,7 +22,9 @@ leg may import this package. It shares no code with the HIP library and never
 imports it; the product path never imports this package.
 
 Parity status: attention, layouts and block copies are pinned against
-independent routines (tests/test_oracle_*.py); scheduling by hand-worked
+independent routines (tests/test_oracle_*.py); the invariant checks by
+hand-built states that break each invariant and must be rejected
+(tests/test_oracle_invariants.py); scheduling by hand-worked
 placements and by the competitive bound of Appendix C checked against
 brute-force optima (tests/test_sched.py). The reclaim policy details that
 the paper leaves open (which slots the lender takes back, how the victim is
@@ -33,7 +35,8 @@ from .layout import LAYOUT_ATTN, LAYOUT_NHD, block_bytes, decode_block, encode_b
 from .slice_state import (SliceOracle, OracleError, FREE, STAGING, LENDER, LOCAL, SLICE,
                           ERR_INVAL, ERR_NOMEM, ERR_OWNER)
 from .attention import paged_decode_attention, contiguous_decode_attention
-from .invariants import check_ownership, check_conservation, check_sd_symmetry, logical_view
+from .invariants import (InvariantError, check_ownership, check_conservation, check_sd_symmetry,
+                         logical_view)
 from .sched import SchedOracle
 
 __all__ = [
@@ -41,5 +44,5 @@ __all__ = [
     "to_float64", "SliceOracle", "OracleError", "FREE", "STAGING", "LENDER", "LOCAL", "SLICE",
     "ERR_INVAL", "ERR_NOMEM", "ERR_OWNER", "paged_decode_attention",
     "contiguous_decode_attention", "check_ownership", "check_conservation",
-    "check_sd_symmetry", "logical_view", "SchedOracle",
+    "check_sd_symmetry", "logical_view", "InvariantError", "SchedOracle",
 ]
