@@ -40,7 +40,9 @@
  *   streams is the caller's job (events).
  *   A handle is not thread-safe. Attention calls on one handle share its
  *   split-K workspace: do not run two of them concurrently on different
- *   streams.
+ *   streams. Reclaim and run prefetches share the handle's plan upload area
+ *   and order themselves on the device (a later call's stream waits for the
+ *   earlier call's kernels), so they may be issued on different streams.
  *   Device paths support head_dim 128 and block_size in {16,32,64,128,256}.
  *   Device id arrays are validated on the host only when the slice was
  *   created with EMA_CREATE_CHECKED (it costs a device-to-host copy). Without
@@ -66,6 +68,7 @@ extern "C" {
 
 #define EMA_F16 0
 #define EMA_BF16 1
+#define EMA_F32 2    /* attention output only */
 
 #define EMA_LAYOUT_ATTN 0
 #define EMA_LAYOUT_NHD 1
@@ -79,6 +82,7 @@ extern "C" {
 
 #define EMA_CREATE_HOST_ONLY 1u  /* bookkeeping only: no device memory, no kernels */
 #define EMA_CREATE_CHECKED 2u    /* validate device id arrays on the host          */
+#define EMA_CREATE_ATTN_GRID 4u  /* attention always in the grid form (see there)  */
 
 typedef struct ema_slice* ema_slice_t;
 
@@ -115,12 +119,14 @@ typedef struct {
  * is reserved jointly and its segments are assigned one user at a time).
  * Allocates two separate device regions on the current HIP device:
  * floor(local_bytes/block_bytes) local blocks and floor(lent_bytes/block_bytes)
- * slice slots, all FREE, lim = n_slice (everything lent), plus reclaim's plan
- * buffers (8 bytes per block, pinned host and device), so that reclaim itself
- * never allocates.
+ * slice slots, all FREE, lim = n_slice (everything lent), plus the plan
+ * upload area of reclaim and run prefetches (16 bytes per block, pinned host
+ * and device) and the stream-K attention workspace (partials of one
+ * workgroup per compute unit, combine records for 4096 sequences), so that
+ * neither reclaim nor stream-K attention ever allocates.
  * flags: EMA_CREATE_HOST_ONLY (no device memory; copy and attention entry
- * points then take host id arrays, validate them and launch nothing) and/or
- * EMA_CREATE_CHECKED.
+ * points then take host id arrays, validate them and launch nothing),
+ * EMA_CREATE_CHECKED, EMA_CREATE_ATTN_GRID.
  * Errors: INVAL (shape out of the supported range, NULL out), HIP (device
  * allocation failed; nothing is leaked).
  */
@@ -188,20 +194,24 @@ int ema_slice_prefetch(ema_slice_t h, const int32_t* block_ids, const int32_t* d
  * gather kernel (any slice layout); EMA_ENGINE_DMA issues one device-to-device
  * transfer per run on the copy engines, leaving the compute units free (slice
  * in EMA_LAYOUT_ATTN only: the engines copy bytes as they are). The list
- * upload shares the reclaim plan buffer and first waits for its previous
- * upload. Async on `stream`. Errors: INVAL (validated on the host in every
- * mode), HIP.
+ * upload uses the handle's plan upload area (see the conventions above).
+ * Async on `stream`. Errors: INVAL (validated on the host in every mode),
+ * HIP.
  */
 int ema_slice_prefetch_runs(ema_slice_t h, const int32_t* src_first, const int32_t* dst_first,
                             const int32_t* run_blocks, int32_t n_runs, int32_t engine,
                             void* stream);
 
 /*
- * Moves logical blocks between pools: block dst_ids[i] <- block src_ids[i]
- * (device [n] unified ids; each destination already allocated to the
- * source's owner; no duplicate destinations; sources and destinations
- * disjoint), re-laid into the destination pool's layout. The caller then
- * frees the sources and updates its tables. Async on `stream`.
+ * slice_migrate -- moves logical blocks between pools, the borrower-side step of
+ * dynamic sharing (section 4: segments are assigned to a user on demand and
+ * may be reassigned over time; section 4.1: allocation first tries free
+ * memory, so a block placed locally can later move into a lent slot and
+ * back). Block dst_ids[i] <- block src_ids[i] (device [n] unified ids; each
+ * destination already allocated to the source's owner; no duplicate
+ * destinations; sources and destinations disjoint), re-laid into the
+ * destination pool's layout. The caller then frees the sources and updates
+ * its tables. Async on `stream`.
  * Errors (checked mode or host-only): INVAL.
  */
 int ema_slice_migrate(ema_slice_t h, const int32_t* src_ids, const int32_t* dst_ids, int32_t n,
@@ -222,7 +232,9 @@ int ema_slice_writeback(ema_slice_t h, const int32_t* staging_ids, const int32_t
 
 /*
  * kv_append -- a decode step stores each sequence's new token before attention
- * reads it: for sequence b with seq_lens[b] > 0 (lengths already counting the
+ * reads it (section 2.3 and 4.2.2: decode appends to the KV cache every step,
+ * and data swapped in through the swap buffer must later be swapped out; the
+ * append lands in the staged copy that the swap-out returns): for sequence b with seq_lens[b] > 0 (lengths already counting the
  * new token), the token at position p = seq_lens[b] - 1 gets K = k_new[b] and
  * V = v_new[b] in row p % block_size of local block block_table[b][p /
  * block_size]. block_table is an attention table (device [batch][max_blocks]
@@ -257,10 +269,13 @@ int ema_kv_append(ema_slice_t h, const void* k_new, const void* v_new, const int
  * preempted owners in order; moves_src/moves_dst (host [moves_cap], may be
  * NULL): the copies made. Counts beyond a cap are still reported in result.
  * In host-only mode canon_tables must be NULL with n_entries 0.
- * The plan (8 bytes per moved or released block) is uploaded from the
- * handle's pinned buffer; a reclaim first waits for the previous upload from
- * that buffer (a reclaim's, or a kernel-engine run prefetch's) to finish,
- * never for anything else on the device.
+ * Device work: one upload of the plan (4 bytes per mover twice, per slot of
+ * the returned range, per released block outside it) from the handle's
+ * pinned buffer, then one launch that copies the movers and, in its first
+ * workgroups, rewrites the tables. The upload area is shared with run
+ * prefetches (see the conventions above): before overwriting it, a reclaim
+ * waits on the host for the previous upload to leave the pinned buffer and
+ * makes `stream` wait for the kernels that read the previous plan.
  * Errors: INVAL (n_blocks < 0, n_entries < 0, bad table pointer), HIP. The
  * bookkeeping changes before the copies are enqueued: after a HIP error the
  * ownership and lim already reflect the plan, while the copies and the table
@@ -282,15 +297,25 @@ int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, in
  * block_table: device int32 [batch][max_blocks] local ids (slice ids are an
  * error; read the prefetched staging copies instead). seq_lens: device int32
  * [batch], each <= max_blocks*block_size; 0 gives zeros. scale <= 0 means
- * 1/sqrt(head_dim). out: device float32 [batch][num_q_heads][head_dim].
+ * 1/sqrt(head_dim). out: device [batch][num_q_heads][head_dim] of out_dtype:
+ * EMA_F32 (fp32 accumulation stored as is), or EMA_BF16 / EMA_F16 (the same
+ * fp32 result rounded to nearest even).
  * The result does not depend on which local blocks hold the tokens, bit for
  * bit. Async on `stream`.
+ * Scheduling: stream-K over all (sequence, KV head) pairs when batch <= 4096
+ * (2048 at 16 query heads per KV head), in the workspace allocated at create;
+ * otherwise, or with EMA_CREATE_ATTN_GRID, a grid of 1024-token chunks whose
+ * split-K workspace grows on first use (which synchronizes the device, frees
+ * the smaller workspace -- graphs captured earlier with grid-form calls must
+ * not be replayed afterwards -- and is refused while `stream` is capturing).
  * Errors: INVAL (num_q_heads not a multiple of num_kv_heads or group > 16,
- * batch/max_blocks < 0, unsupported shape), HIP.
+ * batch/max_blocks < 0, unsupported shape or out_dtype, workspace growth
+ * during capture), HIP.
  */
 int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* block_table,
                                const int32_t* seq_lens, int32_t batch, int32_t num_q_heads,
-                               int32_t max_blocks, float scale, float* out, void* stream);
+                               int32_t max_blocks, float scale, void* out, int32_t out_dtype,
+                               void* stream);
 
 /*
  * Synchronizes the device, then reads and clears the number of ids the

@@ -7,6 +7,7 @@
 // one thread per channel, merging 16 splits per memory round trip with an
 // online rescale; no barriers. Summation order depends only on the number of
 // splits.
+#include "attn_store.h"
 #include "kernels.h"
 
 #include <cmath>
@@ -58,7 +59,7 @@ __global__ __launch_bounds__(kD) void attn_combine_kernel(AttnArgs a) {
     }
     M = Mb;
   }
-  a.out[(int64_t(b) * a.q_heads + hq) * kD + tid] = L > 0.0f ? O / L : 0.0f;
+  store_out(a, (int64_t(b) * a.q_heads + hq) * kD + tid, L > 0.0f ? O / L : 0.0f);
 }
 
 }  // namespace

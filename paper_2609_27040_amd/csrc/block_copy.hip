@@ -65,15 +65,46 @@ __device__ __forceinline__ void wave_lds_sync() {
   __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 }
 
+// The table-rewrite share of a reclaim launch: workgroup g rewrites entries
+// [g * kRewriteEntries, (g + 1) * kRewriteEntries), threads strided so that
+// reads and writes stay coalesced. Only changed entries are written.
+__device__ __forceinline__ void rewrite_tables(const TableRewrite& rw, int g) {
+  const int64_t e0 = int64_t(g) * kRewriteEntries;
+  const int64_t e1 = e0 + kRewriteEntries < rw.n_entries ? e0 + kRewriteEntries : rw.n_entries;
+  for (int64_t e = e0 + threadIdx.x; e < e1; e += blockDim.x) {
+    const int32_t t = rw.tables[e];
+    if (t < 0) continue;
+    int32_t nt = t;
+    const uint32_t r = uint32_t(t - rw.base);
+    if (r < uint32_t(rw.n_range)) {
+      nt = rw.range_map[r];
+    } else if (rw.n_victims > 0) {
+      int lo = 0, hi = rw.n_victims;               // first victim >= t
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (rw.victims[mid] < t) lo = mid + 1;
+        else hi = mid;
+      }
+      if (lo < rw.n_victims && rw.victims[lo] == t) nt = -1;
+    }
+    if (nt != t) rw.tables[e] = nt;
+  }
+}
+
 __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
                                                          const int32_t* __restrict__ src_ids,
                                                          const int32_t* __restrict__ dst_ids,
-                                                         int32_t n, int32_t* err_count) {
+                                                         int32_t n, int32_t* err_count,
+                                                         TableRewrite rw) {
   extern __shared__ __attribute__((aligned(16))) uint16_t lds_tile[];
+  if (int(blockIdx.x) < rw.n_groups) {
+    rewrite_tables(rw, blockIdx.x);
+    return;
+  }
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int upb = int(pv.block_bytes / kUnitBytes);
-  const int64_t unit = int64_t(blockIdx.x) * kWaves + wave;
+  const int64_t unit = (int64_t(blockIdx.x) - rw.n_groups) * kWaves + wave;
   if (unit >= int64_t(n) * upb) return;
   const int32_t i = int32_t(unit / upb);
   const int k = int(unit - int64_t(i) * upb);
@@ -230,10 +261,16 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
 __global__ __launch_bounds__(256) void block_copy_same_kernel(PoolView pv,
                                                               const int32_t* __restrict__ src_ids,
                                                               const int32_t* __restrict__ dst_ids,
-                                                              int32_t n, int32_t* err_count) {
+                                                              int32_t n, int32_t* err_count,
+                                                              TableRewrite rw) {
+  if (int(blockIdx.x) < rw.n_groups) {
+    rewrite_tables(rw, blockIdx.x);
+    return;
+  }
   const int lane = threadIdx.x & 63;
   const int ppb = int(pv.block_bytes / kPieceBytes);
-  const int64_t piece = int64_t(blockIdx.x) * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  const int64_t piece =
+      (int64_t(blockIdx.x) - rw.n_groups) * (blockDim.x >> 6) + (threadIdx.x >> 6);
   if (piece >= int64_t(n) * ppb) return;
   const int32_t i = int32_t(piece / ppb);
   const int k = int(piece - int64_t(i) * ppb);
@@ -284,57 +321,42 @@ __global__ __launch_bounds__(128) void kv_append_kernel(PoolView pv, const uint1
   blk[int64_t(BS) * H * 128 + (int64_t(h) * 128 + d) * BS + r] = v_new[src];
 }
 
-__global__ void remap_scatter_kernel(int32_t* __restrict__ remap, int32_t n_total,
-                                     const int32_t* __restrict__ keys,
-                                     const int32_t* __restrict__ vals, int32_t n) {
-  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const int32_t key = keys[i];
-  if (key >= 0 && key < n_total) remap[key] = vals[i];
-}
-
-__global__ void iota_kernel(int32_t* __restrict__ remap, int32_t n) {
-  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) remap[i] = i;
-}
-
-__global__ void table_rewrite_kernel(int32_t* __restrict__ tables, int64_t n_entries,
-                                     const int32_t* __restrict__ remap, int32_t n_total) {
-  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
-  for (int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; e < n_entries; e += stride) {
-    const int32_t t = tables[e];
-    if (t >= 0 && t < n_total) {
-      const int32_t nt = remap[t];
-      if (nt != t) tables[e] = nt;
-    }
-  }
-}
-
 }  // namespace
 
 hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32_t* dst,
-                             int32_t n, int32_t* err_count, hipStream_t stream, bool runs) {
-  if (n <= 0) return hipSuccess;
+                             int32_t n, int32_t* err_count, hipStream_t stream, bool runs,
+                             const TableRewrite* rw) {
+  TableRewrite rwl;
+  if (rw && rw->n_entries > 0) {
+    rwl = *rw;
+    rwl.n_groups = int32_t((rw->n_entries + kRewriteEntries - 1) / kRewriteEntries);
+  }
+  if (n <= 0 && rwl.n_groups == 0) return hipSuccess;
   const bool same = pv.slice_layout == 0;
   const int64_t upb = pv.block_bytes / (same ? kPieceBytes : kUnitBytes);   // waves per block
   const int wg_waves =
       same && !runs && pv.block_bytes <= 65536 && int64_t(n) * upb <= (int64_t(1) << 22) ? 1
                                                                                         : kWaves;
   const size_t lds = same ? 0 : size_t(kWaves) * tile_elems(pv.block_size) * 2;
-  // A launch stays below 2^32 work-items: at most 2^25 wavefronts.
+  // A launch stays below 2^32 work-items: at most 2^25 wavefronts. The table
+  // rewrite rides on the first launch.
   const int64_t max_blocks = std::max<int64_t>(1, (int64_t(1) << 25) / upb);
-  for (int64_t b0 = 0; b0 < n; b0 += max_blocks) {
-    const int32_t m = int32_t(std::min<int64_t>(max_blocks, n - b0));
-    const int64_t grid = (int64_t(m) * upb + wg_waves - 1) / wg_waves;
+  int64_t b0 = 0;
+  do {
+    const int32_t m = int32_t(std::max<int64_t>(0, std::min<int64_t>(max_blocks, n - b0)));
+    const int64_t grid = (int64_t(m) * upb + wg_waves - 1) / wg_waves + rwl.n_groups;
+    const unsigned threads = same ? unsigned(64 * wg_waves) : 256u;
     if (same)
-      hipLaunchKernelGGL(block_copy_same_kernel, dim3(unsigned(grid)), dim3(64 * wg_waves), 0,
-                         stream, pv, src + b0, dst + b0, m, err_count);
+      hipLaunchKernelGGL(block_copy_same_kernel, dim3(unsigned(grid)), dim3(threads), 0, stream,
+                         pv, src + b0, dst + b0, m, err_count, rwl);
     else
-      hipLaunchKernelGGL(block_copy_kernel, dim3(unsigned(grid)), dim3(256), lds, stream, pv,
-                         src + b0, dst + b0, m, err_count);
+      hipLaunchKernelGGL(block_copy_kernel, dim3(unsigned(grid)), dim3(threads), lds, stream, pv,
+                         src + b0, dst + b0, m, err_count, rwl);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-  }
+    rwl.n_groups = 0;
+    b0 += m;
+  } while (b0 < n);
   return hipSuccess;
 }
 
@@ -345,30 +367,6 @@ hipError_t launch_kv_append(const PoolView& pv, const void* k_new, const void* v
   hipLaunchKernelGGL(kv_append_kernel, dim3(unsigned(batch), unsigned(pv.kv_heads)), dim3(128), 0,
                      stream, pv, static_cast<const uint16_t*>(k_new),
                      static_cast<const uint16_t*>(v_new), table, seq_lens, max_blocks, err_count);
-  return hipGetLastError();
-}
-
-hipError_t launch_remap_scatter(int32_t* remap, int32_t n_total, const int32_t* keys,
-                                const int32_t* vals, int32_t n, hipStream_t stream) {
-  if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(remap_scatter_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, remap,
-                     n_total, keys, vals, n);
-  return hipGetLastError();
-}
-
-hipError_t launch_iota(int32_t* remap, int32_t n, hipStream_t stream) {
-  if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(iota_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, remap, n);
-  return hipGetLastError();
-}
-
-hipError_t launch_table_rewrite(int32_t* tables, int64_t n_entries, const int32_t* remap,
-                                int32_t n_total, hipStream_t stream) {
-  if (n_entries <= 0) return hipSuccess;
-  int64_t grid = (n_entries + 255) / 256;
-  if (grid > 8192) grid = 8192;
-  hipLaunchKernelGGL(table_rewrite_kernel, dim3(unsigned(grid)), dim3(256), 0, stream, tables,
-                     n_entries, remap, n_total);
   return hipGetLastError();
 }
 

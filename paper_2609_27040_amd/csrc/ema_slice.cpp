@@ -1,12 +1,13 @@
 // C ABI of the memory-slice hot path (declared in include/ema_slice.h).
 //
 // One handle = host bookkeeping (SliceBook) + two separately allocated device
-// pools + library scratch: an identity remap of all unified ids used by
-// reclaim's table rewrite, a kernel error counter, an upload area for the copy
-// lists that reclaim and run prefetches build on the host (with its pinned
-// host staging; both sized at create for every block once), and the attention
-// split-K workspace, which grows on first use (growing synchronizes the
-// device).
+// pools + library scratch, all allocated at create: a kernel error counter, an
+// upload area for the plans and copy lists that reclaim and run prefetches
+// build on the host (with its pinned host staging, sized for the largest
+// plan), and the stream-K attention workspace (partials and combine records
+// for the largest batch the stream-K form takes). Only the grid form of
+// attention (batches above the stream-K limit, or EMA_CREATE_ATTN_GRID) grows
+// a workspace on first use; growing synchronizes the device.
 #include "ema_slice.h"
 
 #include <hip/hip_runtime.h>
@@ -33,20 +34,22 @@ struct ema_slice {
   ema::SliceBook book;
   char* local = nullptr;
   char* slice = nullptr;
-  int32_t* d_remap = nullptr;
   int32_t* d_err = nullptr;
   int32_t* d_work = nullptr;
   size_t work_cap = 0;          // ints
   int32_t* h_work = nullptr;    // pinned
   size_t h_work_cap = 0;        // ints
-  hipEvent_t h_work_ev = nullptr;
+  hipEvent_t h_work_ev = nullptr;   // after the last upload from h_work
   bool h_work_pending = false;
-  float* d_part = nullptr;
-  size_t part_cap = 0;          // floats
-  int32_t* d_info = nullptr;      // stream-K: per (sequence, KV head) partial ranges
-  size_t info_cap = 0;            // ints
-  bool attn_valu = false;         // EMA_ATTN_KERNEL=valu selects the vector-ALU kernel
-  bool attn_grid = false;         // EMA_ATTN_SCHED=grid forces the matrix-core grid form
+  hipEvent_t d_work_ev = nullptr;   // after the last kernel that read d_work
+  bool d_work_pending = false;
+  float* d_part = nullptr;          // stream-K partial slots (fixed size)
+  size_t part_cap = 0;              // floats
+  int32_t* d_info = nullptr;        // stream-K: per (sequence, KV head) partial ranges
+  size_t info_cap = 0;              // ints
+  float* d_gpart = nullptr;         // grid form: split-K partials (grows)
+  size_t gpart_cap = 0;             // floats
+  bool attn_grid = false;           // EMA_CREATE_ATTN_GRID: always the grid form
 };
 
 namespace {
@@ -145,8 +148,13 @@ int fetch_ints(const int32_t* dev, int64_t n, hipStream_t st, std::vector<int32_
   return EMA_OK;
 }
 
-int grow_device(void** p, size_t* cap, size_t need, size_t elem) {
+int grow_device(void** p, size_t* cap, size_t need, size_t elem, hipStream_t st) {
   if (need <= *cap) return EMA_OK;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  HIP_TRY(hipStreamIsCapturing(st, &cs), "hipStreamIsCapturing");
+  if (cs != hipStreamCaptureStatusNone)
+    return fail(EMA_ERR_INVAL, "attention: the grid-form workspace would grow during stream "
+                               "capture; run a call of this size once before capturing");
   HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize(grow)");
   if (*p) HIP_TRY(hipFree(*p), "hipFree(grow)");
   *p = nullptr;
@@ -162,15 +170,44 @@ void release(ema_slice* h) {
     (void)hipDeviceSynchronize();
     if (h->local) (void)hipFree(h->local);
     if (h->slice) (void)hipFree(h->slice);
-    if (h->d_remap) (void)hipFree(h->d_remap);
     if (h->d_err) (void)hipFree(h->d_err);
     if (h->d_work) (void)hipFree(h->d_work);
     if (h->d_part) (void)hipFree(h->d_part);
     if (h->d_info) (void)hipFree(h->d_info);
+    if (h->d_gpart) (void)hipFree(h->d_gpart);
     if (h->h_work) (void)hipHostFree(h->h_work);
     if (h->h_work_ev) (void)hipEventDestroy(h->h_work_ev);
+    if (h->d_work_ev) (void)hipEventDestroy(h->d_work_ev);
   }
   delete h;
+}
+
+// The plan upload area (h_work -> d_work) is shared by reclaim and run
+// prefetches, which may be issued on different streams. begin_upload waits on
+// the host until the previous upload has left h_work, and makes `st` wait on
+// the device until the previous kernels that read d_work have finished;
+// end_upload marks the point after this call's kernels.
+int begin_upload(ema_slice* h, hipStream_t st) {
+  if (h->h_work_pending) {
+    HIP_TRY(hipEventSynchronize(h->h_work_ev), "hipEventSynchronize(upload)");
+    h->h_work_pending = false;
+  }
+  if (h->d_work_pending) HIP_TRY(hipStreamWaitEvent(st, h->d_work_ev, 0), "hipStreamWaitEvent");
+  return EMA_OK;
+}
+
+int upload(ema_slice* h, size_t n_ints, hipStream_t st) {
+  HIP_TRY(hipMemcpyAsync(h->d_work, h->h_work, n_ints * 4, hipMemcpyHostToDevice, st),
+          "hipMemcpyAsync(upload)");
+  HIP_TRY(hipEventRecord(h->h_work_ev, st), "hipEventRecord(upload)");
+  h->h_work_pending = true;
+  return EMA_OK;
+}
+
+int end_upload(ema_slice* h, hipStream_t st) {
+  HIP_TRY(hipEventRecord(h->d_work_ev, st), "hipEventRecord(kernels)");
+  h->d_work_pending = true;
+  return EMA_OK;
 }
 
 }  // namespace
@@ -188,7 +225,7 @@ int ema_slice_create(const ema_kv_shape* shape, size_t local_bytes, size_t lent_
       (shape->dtype != EMA_F16 && shape->dtype != EMA_BF16) ||
       (shape->slice_layout != EMA_LAYOUT_ATTN && shape->slice_layout != EMA_LAYOUT_NHD))
     return fail(EMA_ERR_INVAL, "create: unsupported shape");
-  if (flags & ~(EMA_CREATE_HOST_ONLY | EMA_CREATE_CHECKED))
+  if (flags & ~(EMA_CREATE_HOST_ONLY | EMA_CREATE_CHECKED | EMA_CREATE_ATTN_GRID))
     return fail(EMA_ERR_INVAL, "create: unknown flags");
   const int64_t bb = 2LL * shape->block_size * shape->num_kv_heads * shape->head_dim * 2;
   const uint64_t nl = local_bytes / uint64_t(bb), ns = lent_bytes / uint64_t(bb);
@@ -202,10 +239,7 @@ int ema_slice_create(const ema_kv_shape* shape, size_t local_bytes, size_t lent_
   h->bb = bb;
   h->host_only = (flags & EMA_CREATE_HOST_ONLY) != 0;
   h->checked = (flags & EMA_CREATE_CHECKED) != 0;
-  const char* impl = std::getenv("EMA_ATTN_KERNEL");
-  h->attn_valu = impl && std::strcmp(impl, "valu") == 0;
-  const char* sched = std::getenv("EMA_ATTN_SCHED");
-  h->attn_grid = sched && std::strcmp(sched, "grid") == 0;
+  h->attn_grid = (flags & EMA_CREATE_ATTN_GRID) != 0;
   h->book.init(int32_t(nl), int32_t(ns));
   if (h->host_only) {
     *out = guard.release();
@@ -215,18 +249,25 @@ int ema_slice_create(const ema_kv_shape* shape, size_t local_bytes, size_t lent_
   const int32_t n_total = int32_t(nl + ns);
   if (e == hipSuccess && nl) e = hipMalloc(&h->local, nl * bb);
   if (e == hipSuccess && ns) e = hipMalloc(&h->slice, ns * bb);
-  if (e == hipSuccess && n_total) e = hipMalloc(&h->d_remap, size_t(n_total) * 4);
   if (e == hipSuccess) e = hipMalloc(&h->d_err, 4);
   if (e == hipSuccess) e = hipMemset(h->d_err, 0, 4);
-  if (e == hipSuccess) e = ema::launch_iota(h->d_remap, n_total, nullptr);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&h->h_work_ev, hipEventDisableTiming);
-  // Reclaim's plan upload: keys and values of at most every block once
-  // (movers and released blocks are disjoint), so reclaim never allocates.
-  const size_t work = size_t(2) * size_t(n_total > 0 ? n_total : 1);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&h->d_work_ev, hipEventDisableTiming);
+  // Reclaim's plan upload (movers' sources and destinations, the returned
+  // range's remap, the released blocks outside it: at most 4 ints per block)
+  // and run prefetches' block lists (2 per block), so neither ever allocates.
+  const size_t work = size_t(4) * size_t(n_total > 0 ? n_total : 1) + 16;
   if (e == hipSuccess) e = hipHostMalloc(&h->h_work, work * 4, hipHostMallocDefault);
   if (e == hipSuccess) h->h_work_cap = work;
   if (e == hipSuccess) e = hipMalloc(&h->d_work, work * 4);
   if (e == hipSuccess) h->work_cap = work;
+  // Stream-K attention workspace for every head count and the largest batch.
+  const size_t part = size_t(2) * ema::attn_streamk_grid() * ema::kMaxGroup * (ema::kHeadDim + 2);
+  const size_t info = size_t(ema::streamk_max_batch(1)) * shape->num_kv_heads * 3;
+  if (e == hipSuccess) e = hipMalloc(&h->d_part, part * 4);
+  if (e == hipSuccess) h->part_cap = part;
+  if (e == hipSuccess) e = hipMalloc(&h->d_info, info * 4);
+  if (e == hipSuccess) h->info_cap = info;
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) return hip_fail(e, "create");   // the guard releases h
   *out = guard.release();
@@ -403,21 +444,15 @@ int ema_slice_prefetch_runs(ema_slice_t h, const int32_t* src_first, const int32
     }
     return EMA_OK;
   }
-  if (h->h_work_pending) {
-    HIP_TRY(hipEventSynchronize(h->h_work_ev), "hipEventSynchronize(runs)");
-    h->h_work_pending = false;
-  }
   if (size_t(2) * n > h->h_work_cap || size_t(2) * n > h->work_cap)
     return fail(EMA_ERR_INVAL, "prefetch_runs: more blocks than the plan buffer holds");
+  if ((rc = begin_upload(h, st))) return rc;
   std::copy(src.begin(), src.end(), h->h_work);
   std::copy(dst.begin(), dst.end(), h->h_work + n);
-  HIP_TRY(hipMemcpyAsync(h->d_work, h->h_work, size_t(2) * n * 4, hipMemcpyHostToDevice, st),
-          "hipMemcpyAsync(runs)");
-  HIP_TRY(hipEventRecord(h->h_work_ev, st), "hipEventRecord(runs)");
-  h->h_work_pending = true;
+  if ((rc = upload(h, size_t(2) * n, st))) return rc;
   HIP_TRY(ema::launch_block_copy(pool_view(h), h->d_work, h->d_work + n, n, h->d_err, st, true),
           "prefetch_runs launch");
-  return EMA_OK;
+  return end_upload(h, st);
 } catch (...) {
   return internal_error();
 }
@@ -505,51 +540,57 @@ int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, in
   const bool rewrite = n_entries > 0 && (m > 0 || nv > 0);
   if (m == 0 && !rewrite) return EMA_OK;
 
-  // Upload area: keys[m+nv] | vals[m+nv] | (moves are keys[0..m) -> vals[0..m)).
+  // Upload: move sources [m] | destinations [m] | remap of the returned range
+  // [n'] | released blocks outside the range, ascending [nvo]. One launch then
+  // copies the movers and (its first workgroups) rewrites the tables.
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const int32_t np = m + nv;
-  const size_t need = size_t(2) * np;
-  if (h->h_work_pending) {
-    HIP_TRY(hipEventSynchronize(h->h_work_ev), "hipEventSynchronize(reclaim)");
-    h->h_work_pending = false;
-  }
-  // movers and released blocks are disjoint, so np <= n_total and the
-  // buffers sized at create always hold the plan
+  const int32_t n_range = plan.reclaimed;
+  const int32_t base = h->book.n_local() + plan.cut;
+  std::vector<int32_t> vout;
+  for (int32_t u : plan.victim_blocks)
+    if (u < base || u >= base + n_range) vout.push_back(u);
+  std::sort(vout.begin(), vout.end());
+  const int32_t nvo = int32_t(vout.size());
+  const size_t need = size_t(2) * m + (rewrite ? size_t(n_range) + nvo : 0);
+  // movers, the range and released blocks are within n_total, so the buffers
+  // sized at create always hold the plan
   if (need > h->h_work_cap || need > h->work_cap)
     return fail(EMA_ERR_INVAL, "reclaim: plan larger than the work buffers");
-  int32_t* keys = h->h_work;
-  int32_t* vals = h->h_work + np;
-  for (int32_t i = 0; i < m; ++i) {
-    keys[i] = plan.move_src[i];
-    vals[i] = plan.move_dst[i];
-  }
-  for (int32_t i = 0; i < nv; ++i) {
-    keys[m + i] = plan.victim_blocks[i];
-    vals[m + i] = -1;
-  }
-  HIP_TRY(hipMemcpyAsync(h->d_work, h->h_work, need * 4, hipMemcpyHostToDevice, st),
-          "hipMemcpyAsync(reclaim)");
-  HIP_TRY(hipEventRecord(h->h_work_ev, st), "hipEventRecord");
-  h->h_work_pending = true;
-  const int32_t* dkeys = h->d_work;
-  const int32_t* dvals = h->d_work + np;
-  const ema::PoolView pv = pool_view(h);
-  const int32_t n_total = pv.n_local + pv.n_slice;
-  HIP_TRY(ema::launch_block_copy(pv, dkeys, dvals, m, h->d_err, st, true), "reclaim copy");
+  if ((rc = begin_upload(h, st))) return rc;
+  int32_t* w = h->h_work;
+  std::copy(plan.move_src.begin(), plan.move_src.end(), w);
+  std::copy(plan.move_dst.begin(), plan.move_dst.end(), w + m);
   if (rewrite) {
-    HIP_TRY(ema::launch_remap_scatter(h->d_remap, n_total, dkeys, dvals, np, st), "remap set");
-    HIP_TRY(ema::launch_table_rewrite(canon_tables, n_entries, h->d_remap, n_total, st),
-            "table rewrite");
-    HIP_TRY(ema::launch_remap_scatter(h->d_remap, n_total, dkeys, dkeys, np, st), "remap reset");
+    int32_t* rmap = w + 2 * size_t(m);
+    for (int32_t i = 0; i < n_range; ++i) rmap[i] = base + i;
+    for (int32_t i = 0; i < m; ++i) rmap[plan.move_src[i] - base] = plan.move_dst[i];
+    for (int32_t u : plan.victim_blocks)
+      if (u >= base && u < base + n_range) rmap[u - base] = -1;
+    std::copy(vout.begin(), vout.end(), rmap + n_range);
   }
-  return EMA_OK;
+  if ((rc = upload(h, need, st))) return rc;
+  ema::TableRewrite rw;
+  if (rewrite) {
+    rw.tables = canon_tables;
+    rw.n_entries = n_entries;
+    rw.range_map = h->d_work + 2 * size_t(m);
+    rw.victims = h->d_work + 2 * size_t(m) + n_range;
+    rw.base = base;
+    rw.n_range = n_range;
+    rw.n_victims = nvo;
+  }
+  HIP_TRY(ema::launch_block_copy(pool_view(h), h->d_work, h->d_work + m, m, h->d_err, st, true,
+                                 &rw),
+          "reclaim launch");
+  return end_upload(h, st);
 } catch (...) {
   return internal_error();
 }
 
 int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* block_table,
                                const int32_t* seq_lens, int32_t batch, int32_t num_q_heads,
-                               int32_t max_blocks, float scale, float* out, void* stream) try {
+                               int32_t max_blocks, float scale, void* out, int32_t out_dtype,
+                               void* stream) try {
   if (!h) return fail(EMA_ERR_INVAL, "attention: NULL handle");
   const int32_t hkv = h->shape.num_kv_heads;
   if (batch < 0 || max_blocks < 0 || num_q_heads < hkv || num_q_heads % hkv != 0)
@@ -557,6 +598,8 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
   const int32_t G = num_q_heads / hkv;
   if (G != 1 && G != 2 && G != 4 && G != 8 && G != 16)
     return fail(EMA_ERR_INVAL, "attention: query heads per kv head must be 1, 2, 4, 8 or 16");
+  if (out_dtype != EMA_F32 && out_dtype != EMA_F16 && out_dtype != EMA_BF16)
+    return fail(EMA_ERR_INVAL, "attention: out_dtype must be EMA_F32, EMA_F16 or EMA_BF16");
   if (batch > 65535 || hkv > 65535) return fail(EMA_ERR_INVAL, "attention: grid too large");
   if (batch > 0 && (!q || !block_table || !seq_lens || !out))
     return fail(EMA_ERR_INVAL, "attention: NULL array");
@@ -584,35 +627,40 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
       }
     }
   }
-  // Scheduling. Matrix-core kernel: stream-K (equal tile ranges, one
-  // workgroup per CU, at most two partials each) when the batch fits its LDS work
-  // list, else a grid of 1024-token chunks. Vector-ALU kernel: a grid of
-  // 256-token chunks. Grid forms keep one partial per (sequence, head, chunk).
+  // Scheduling: stream-K (equal tile ranges, one workgroup per CU, at most two
+  // partials each; workspace allocated at create) when the batch fits its LDS
+  // work list, else a grid of 1024-token chunks with one partial per
+  // (sequence, head, chunk) in a workspace that grows on first use.
   const int64_t tiles = int64_t(batch) * hkv * ((max_tokens + 31) / 32);
-  const bool stream_k = !h->attn_valu && !h->attn_grid && batch <= ema::streamk_max_batch(G) &&
-                        tiles < (int64_t(1) << 30);
-  const int32_t chunk = h->attn_valu ? ema::kAttnChunk : ema::kMfmaGridChunk;
+  const bool stream_k =
+      !h->attn_grid && batch <= ema::streamk_max_batch(G) && tiles < (int64_t(1) << 30);
+  const int32_t chunk = ema::kMfmaGridChunk;
   const int32_t n_split = int32_t(std::max<int64_t>(1, (max_tokens + chunk - 1) / chunk));
   if (!stream_k && n_split > 65535) return fail(EMA_ERR_INVAL, "attention: max_blocks too large");
-  size_t part_rows = 0;
-  if (stream_k)
-    part_rows = size_t(2) * ema::kMaxStreamGrid * G;
-  else if (n_split > 1)
-    part_rows = size_t(batch) * num_q_heads * n_split;
-  if (part_rows &&
-      (rc = grow_device(reinterpret_cast<void**>(&h->d_part), &h->part_cap, part_rows * 130, 4)))
-    return rc;
-  if (stream_k && (rc = grow_device(reinterpret_cast<void**>(&h->d_info), &h->info_cap,
-                                    size_t(batch) * hkv * 3, 4)))
-    return rc;
   ema::AttnArgs a;
+  float* part = nullptr;
+  size_t part_rows = 0;
+  if (stream_k) {
+    part_rows = size_t(2) * ema::attn_streamk_grid() * G;
+    part = h->d_part;
+    a.info = h->d_info;
+  } else {
+    if (n_split > 1) {
+      part_rows = size_t(batch) * num_q_heads * n_split;
+      if ((rc = grow_device(reinterpret_cast<void**>(&h->d_gpart), &h->gpart_cap,
+                            part_rows * (ema::kHeadDim + 2), 4, st)))
+        return rc;
+    }
+    part = h->d_gpart;
+    a.info = nullptr;
+  }
   a.q = q;
   a.table = block_table;
   a.seq_lens = seq_lens;
   a.out = out;
-  a.part_o = h->d_part;
-  a.part_ml = h->d_part ? h->d_part + part_rows * 128 : nullptr;
-  a.info = h->d_info;
+  a.out_dtype = out_dtype;
+  a.part_o = part;
+  a.part_ml = part ? part + part_rows * ema::kHeadDim : nullptr;
   a.stream_k = stream_k ? 1 : 0;
   a.err_count = h->d_err;
   a.local = h->local;
@@ -628,9 +676,7 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
   a.chunk = chunk;
   const float sc = scale > 0.0f ? scale : 1.0f / std::sqrt(float(h->shape.head_dim));
   a.scale_log2 = sc * 1.4426950408889634f;
-  HIP_TRY(h->attn_valu ? ema::launch_paged_attention(a, st)
-                       : ema::launch_paged_attention_mfma(a, st),
-          "attention launch");
+  HIP_TRY(ema::launch_paged_attention_mfma(a, st), "attention launch");
   return EMA_OK;
 } catch (...) {
   return internal_error();

@@ -19,14 +19,33 @@ struct PoolView {
   int32_t slice_layout;  // 0 ATTN, 1 NHD
 };
 
+// Reclaim's table rewrite, done by the first `n_groups` workgroups of the
+// reclaim's copy launch (so the rewrite costs no launch of its own): every
+// entry t of tables[n_entries] with base <= t < base + n_range becomes
+// range_map[t - base] (the mover's destination, -1 for a preempted sequence's
+// block, else t); any other t >= 0 that is in victims[n_victims] (ascending)
+// becomes -1. n_groups == 0: no rewrite.
+struct TableRewrite {
+  int32_t* tables = nullptr;
+  int64_t n_entries = 0;
+  const int32_t* range_map = nullptr;
+  const int32_t* victims = nullptr;
+  int32_t base = 0;
+  int32_t n_range = 0;
+  int32_t n_victims = 0;
+  int32_t n_groups = 0;
+};
+constexpr int kRewriteEntries = 8192;   // table entries per rewriting workgroup
+
 // dst[i] <- src[i] for i < n (unified ids), re-laid between pool layouts.
 // Ids outside [0, n_local + n_slice) are skipped and counted in *err_count.
 // `runs`: the lists are mostly ascending runs of ids (reclaim moves,
 // contiguous-run prefetches) rather than scattered blocks; only the work
-// distribution depends on it.
+// distribution depends on it. `rw` (optional): the table rewrite to run in the
+// same launch (n_groups is set by the launcher).
 hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32_t* dst,
                              int32_t n, int32_t* err_count, hipStream_t stream,
-                             bool runs = false);
+                             bool runs = false, const TableRewrite* rw = nullptr);
 
 // New decode token of every sequence into its block (ATTN layout): row
 // (len-1) % bs of local block table[b][(len-1) / bs], len = seq_lens[b] > 0.
@@ -35,22 +54,11 @@ hipError_t launch_kv_append(const PoolView& pv, const void* k_new, const void* v
                             const int32_t* table, const int32_t* seq_lens, int32_t batch,
                             int32_t max_blocks, int32_t* err_count, hipStream_t stream);
 
-// remap[keys[i]] = vals[i] for i < n (keys checked against n_total).
-hipError_t launch_remap_scatter(int32_t* remap, int32_t n_total, const int32_t* keys,
-                                const int32_t* vals, int32_t n, hipStream_t stream);
-
-// remap[i] = i for i < n.
-hipError_t launch_iota(int32_t* remap, int32_t n, hipStream_t stream);
-
-// t <- remap[t] for every entry 0 <= t < n_total of tables[n_entries].
-hipError_t launch_table_rewrite(int32_t* tables, int64_t n_entries, const int32_t* remap,
-                                int32_t n_total, hipStream_t stream);
-
 struct AttnArgs {
   const void* q;            // [B][Hq][128] 16-bit
   const int32_t* table;     // [B][max_blocks]
   const int32_t* seq_lens;  // [B]
-  float* out;               // [B][Hq][128]
+  void* out;                // [B][Hq][128], out_dtype
   float* part_o;            // [B][Hq][n_split][128] split-K partial outputs
   float* part_ml;           // [B][Hq][n_split][2] running max (log2 domain) and sum
                             // (stream-K: [2 * grid][G][...] partial slots instead)
@@ -62,10 +70,15 @@ struct AttnArgs {
   int32_t batch, q_heads, kv_heads, block_size, max_blocks, n_split, dtype;
   int32_t chunk;            // tokens per split (grid forms)
   int32_t stream_k;         // matrix-core kernel: stream-K scheduling (else grid form)
+  int32_t out_dtype;        // kOutF32, kOutF16 or kOutBF16
   float scale_log2;         // softmax scale times log2(e)
 };
 
-constexpr int kAttnChunk = 256;        // tokens per workgroup of the vector-ALU kernel
+// Output element types (the values of EMA_F16, EMA_BF16, EMA_F32).
+constexpr int kOutF16 = 0;
+constexpr int kOutBF16 = 1;
+constexpr int kOutF32 = 2;
+
 constexpr int kMfmaGridChunk = 1024;   // tokens per workgroup of the matrix-core grid form
 // Sequences the stream-K work list holds in LDS (lengths and prefix sums):
 // sized so that a workgroup's LDS stays within half a CU's 160 KiB, which
@@ -73,9 +86,13 @@ constexpr int kMfmaGridChunk = 1024;   // tokens per workgroup of the matrix-cor
 // merge space, hence the smaller list).
 constexpr int streamk_max_batch(int group) { return group >= 16 ? 2048 : 4096; }
 constexpr int kMaxStreamGrid = 2048;   // stream-K workgroups (partial slots: 2 each)
+constexpr int kHeadDim = 128;          // the only head size the device paths take
+constexpr int kMaxGroup = 16;          // query heads per KV head
+// Stream-K workgroups of every call in this process: one per CU of the device
+// current at the first call, at most kMaxStreamGrid. Partial slots: 2 per
+// workgroup, each kMaxGroup x (kHeadDim + 2) floats at most.
+int attn_streamk_grid();
 
-// Vector-ALU kernel (v_dot2 scores, FMA outputs) plus a separate split-K merge.
-hipError_t launch_paged_attention(const AttnArgs& a, hipStream_t stream);
 // Matrix-core kernel: stream-K when stream_k is set, else the grid form with
 // chunk == kMfmaGridChunk.
 hipError_t launch_paged_attention_mfma(const AttnArgs& a, hipStream_t stream);

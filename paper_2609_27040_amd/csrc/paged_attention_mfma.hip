@@ -32,6 +32,7 @@
 // (past the length, or in a block whose id is out of range) get -inf scores
 // and zeroed V, so NaN in unused slots never leaks.
 // Reduction orders depend only on sequence lengths, not on block ids.
+#include "attn_store.h"
 #include "kernels.h"
 
 #include <algorithm>
@@ -434,7 +435,7 @@ __device__ __forceinline__ void attend_range(const AttnArgs& a, const SegDesc* s
 
 __device__ __forceinline__ void write_zeros(const AttnArgs& a, int b) {
   for (int e = threadIdx.x; e < a.q_heads * kD; e += kThreads)
-    a.out[int64_t(b) * a.q_heads * kD + e] = 0.0f;
+    store_out(a, int64_t(b) * a.q_heads * kD + e, 0.0f);
 }
 
 // Stream-K form. Every workgroup reads all lengths once and prefix-sums the
@@ -589,7 +590,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_streamk(AttnArgs a) {
       const SegDesc& sdd = s_desc[s2];
       const int nt = (sdd.len + kIt - 1) / kIt;
       if (sdd.j0 == 0 && sdd.j1 == nt) {
-        a.out[(int64_t(sdd.b) * a.q_heads + sdd.kvh * G + g) * kD + d] = L > 0.0f ? O / L : 0.0f;
+        store_out(a, (int64_t(sdd.b) * a.q_heads + sdd.kvh * G + g) * kD + d, L > 0.0f ? O / L : 0.0f);
       } else {
         const int64_t slot = int64_t(blockIdx.x) * 2 + (s2 == 0 ? 0 : 1);
         a.part_o[(slot * G + g) * kD + d] = O;
@@ -628,7 +629,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_streamk(AttnArgs a) {
     attend_segment<G, BS, BF16>(a, b, kvh, len, j0, j1, sm,
                                 [&](int g, int d, float M, float L, float O) {
       if (whole) {
-        a.out[(int64_t(b) * a.q_heads + kvh * G + g) * kD + d] = L > 0.0f ? O / L : 0.0f;
+        store_out(a, (int64_t(b) * a.q_heads + kvh * G + g) * kD + d, L > 0.0f ? O / L : 0.0f);
       } else {
         a.part_o[(slot * G + g) * kD + d] = O;
         if (d == 0) {
@@ -673,7 +674,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_grid(AttnArgs a) {
                               [&](int g, int d, float M, float L, float O) {
     const int hq = kvh * G + g;
     if (j0 == 0 && j1 == nt) {
-      a.out[(int64_t(b) * a.q_heads + hq) * kD + d] = L > 0.0f ? O / L : 0.0f;
+      store_out(a, (int64_t(b) * a.q_heads + hq) * kD + d, L > 0.0f ? O / L : 0.0f);
     } else {
       const int64_t row = (int64_t(b) * a.q_heads + hq) * a.n_split + split;
       a.part_o[row * kD + d] = O;
@@ -743,25 +744,14 @@ __global__ __launch_bounds__(kThreads) void attn_combine_streamk(AttnArgs a) {
     merge_partials<4>(a, G, g, d, wa, sa, n, M, L, O);
   else
     merge_partials<16>(a, G, g, d, wa, sa, n, M, L, O);
-  a.out[(int64_t(b) * a.q_heads + kvh * G + g) * kD + d] = L > 0.0f ? O / L : 0.0f;
+  store_out(a, (int64_t(b) * a.q_heads + kvh * G + g) * kD + d, L > 0.0f ? O / L : 0.0f);
 }
 
-// Stream-K grid: one workgroup per CU. A second resident workgroup per CU
-// adds no bandwidth (the two share the CU's memory path, the second running
-// about 20 % slower) but doubles the cut pairs and their partials.
-int streamk_grid() {
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      cus <= 0)
-    return 256;
-  return std::min(cus, kMaxStreamGrid);
-}
 
 template <int G, int BS, bool BF16>
 hipError_t launch_typed(const AttnArgs& a, hipStream_t stream) {
   if (a.stream_k) {
-    static const int grid = streamk_grid();
+    const int grid = attn_streamk_grid();
     hipLaunchKernelGGL((attn_mfma_streamk<G, BS, BF16>), dim3(grid), dim3(kThreads), 0, stream,
                        a);
     hipError_t e = hipGetLastError();
@@ -796,6 +786,21 @@ hipError_t launch_g(const AttnArgs& a, hipStream_t stream) {
 }
 
 }  // namespace
+
+// Stream-K grid: one workgroup per CU. A second resident workgroup per CU
+// adds no bandwidth (the two share the CU's memory path, the second running
+// about 20 % slower) but doubles the cut pairs and their partials.
+int attn_streamk_grid() {
+  static const int grid = [] {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+      return 256;
+    return std::min(cus, kMaxStreamGrid);
+  }();
+  return grid;
+}
 
 hipError_t launch_paged_attention_mfma(const AttnArgs& a, hipStream_t stream) {
   if (a.batch == 0) return hipSuccess;

@@ -18,12 +18,12 @@ import numpy as np
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "libema_slice.so")
 
 OK, ERR_INVAL, ERR_NOMEM, ERR_OWNER, ERR_HIP = 0, -1, -2, -3, -4
-F16, BF16 = 0, 1
+F16, BF16, F32 = 0, 1, 2
 LAYOUT_ATTN, LAYOUT_NHD = 0, 1
 ENGINE_KERNEL, ENGINE_DMA = 0, 1
 POOL_LOCAL, POOL_SLICE = 0, 1
 FREE, STAGING, LENDER = -1, -2, -3
-CREATE_HOST_ONLY, CREATE_CHECKED = 1, 2
+CREATE_HOST_ONLY, CREATE_CHECKED, CREATE_ATTN_GRID = 1, 2, 4
 DTYPES = {"f16": F16, "bf16": BF16}
 
 
@@ -73,7 +73,7 @@ def _load():
         "ema_slice_prefetch_runs": [P, P, P, P, I32, I32, P],
         "ema_kv_append": [P, P, P, P, P, I32, I32, P],
         "ema_slice_reclaim": [P, I32, P, I64, P, ctypes.POINTER(ReclaimResult), P, I32, P, P, I32],
-        "ema_paged_decode_attention": [P, P, P, P, I32, I32, I32, ctypes.c_float, P, P],
+        "ema_paged_decode_attention": [P, P, P, P, I32, I32, I32, ctypes.c_float, P, I32, P],
         "ema_slice_device_errors": [P, ctypes.POINTER(I32)],
         "ema_sched_create": [I32, I32, I64, ctypes.POINTER(P)],
         "ema_sched_destroy": [P],
@@ -179,10 +179,11 @@ def _stream(stream):
 # ---- entry points ---------------------------------------------------------------
 
 def slice_create(num_kv_heads, head_dim, block_size, dtype, slice_layout, local_bytes,
-                 lent_bytes, host_only=False, checked=False):
+                 lent_bytes, host_only=False, checked=False, attn_grid=False):
     shape = KVShape(num_kv_heads, head_dim, block_size, DTYPES.get(dtype, dtype), slice_layout)
     h = ctypes.c_void_p()
-    flags = (CREATE_HOST_ONLY if host_only else 0) | (CREATE_CHECKED if checked else 0)
+    flags = ((CREATE_HOST_ONLY if host_only else 0) | (CREATE_CHECKED if checked else 0)
+             | (CREATE_ATTN_GRID if attn_grid else 0))
     _check(_lib.ema_slice_create(ctypes.byref(shape), int(local_bytes), int(lent_bytes), flags,
                                  ctypes.byref(h)))
     _HANDLES[h.value] = (bool(host_only), shape.dtype, int(num_kv_heads))
@@ -303,17 +304,22 @@ def slice_reclaim(h, n_blocks, canon_tables=None, stream=None, caps=None):
 
 def paged_decode_attention(h, q, block_table, seq_lens, out, scale=0.0, stream=None):
     """q [B][Hq][D] (16-bit), block_table int32 [B][max_blocks], seq_lens int32
-    [B], out float32 [B][Hq][D]: device tensors."""
+    [B], out [B][Hq][D] of float32, float16 or bfloat16 (the output type is
+    the tensor's): device tensors."""
     import torch
     B, Hq = int(q.shape[0]), int(q.shape[1])
     max_blocks = int(block_table.shape[1]) if block_table.dim() == 2 else 0
+    out_types = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
+    if out.dtype not in out_types:
+        _bad(f"out: dtype {out.dtype} not in {tuple(out_types)}")
     if not _host_only(h):
         q = _kv16_dev(h, q, "q", B * Hq * 128)
         block_table = _i32_dev(block_table, "block_table", B * max_blocks)
         seq_lens = _i32_dev(seq_lens, "seq_lens", B)
-        out = _dev(out, "out", (torch.float32,), B * Hq * 128)
+        out = _dev(out, "out", tuple(out_types), B * Hq * 128)
     _check(_lib.ema_paged_decode_attention(h, _ptr(q), _ptr(block_table), _ptr(seq_lens), B, Hq,
-                                           max_blocks, float(scale), _ptr(out), _stream(stream)))
+                                           max_blocks, float(scale), _ptr(out),
+                                           out_types[out.dtype], _stream(stream)))
 
 
 def slice_device_errors(h):

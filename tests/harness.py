@@ -25,7 +25,7 @@ TORCH_DT = {"f16": torch.float16, "bf16": torch.bfloat16}
 class Workload:
     def __init__(self, cfg, layers=None, batch=None, slice_layout=ema.LAYOUT_ATTN, seed=None,
                  staging_slots=2, extra_local=0, extra_slice=0, fill="host", checked=False,
-                 lens=None, frac=None, shuffle=True, stage_n=None, group=1):
+                 lens=None, frac=None, shuffle=True, stage_n=None, group=1, attn_grid=False):
         self.cfg = cfg = cfg if batch is None else cfg.scaled(batch=batch)
         self.L = cfg.layers if layers is None else layers
         rng = np.random.default_rng(cfg.seed if seed is None else seed)
@@ -45,7 +45,8 @@ class Workload:
         n_local = len(pl.local_order) + staging_slots * self.stage_n + extra_local
         n_slice = len(pl.slice_order) + extra_slice
         self.h = ema.slice_create(self.hkv, self.D, self.bs, cfg.dtype, slice_layout,
-                                  n_local * self.bb, n_slice * self.bb, checked=checked)
+                                  n_local * self.bb, n_slice * self.bb, checked=checked,
+                                  attn_grid=attn_grid)
         self.alloc_log = []
         tables = np.full((self.L, self.B, self.maxblk), -1, dtype=np.int64)
         for pool, order in ((ema.POOL_LOCAL, pl.local_order), (ema.POOL_SLICE, pl.slice_order)):

@@ -24,17 +24,11 @@ def ema():
     return m
 
 
-@pytest.fixture(params=["mfma", "mfma-grid", "valu"])
-def impl(request, monkeypatch):
-    """Attention kernel and schedule, chosen when the slice is created: the
-    matrix-core kernel with stream-K scheduling (default), the matrix-core
-    grid form, or the vector-ALU kernel."""
-    monkeypatch.delenv("EMA_ATTN_KERNEL", raising=False)
-    monkeypatch.delenv("EMA_ATTN_SCHED", raising=False)
-    if request.param == "valu":
-        monkeypatch.setenv("EMA_ATTN_KERNEL", "valu")
-    elif request.param == "mfma-grid":
-        monkeypatch.setenv("EMA_ATTN_SCHED", "grid")
+@pytest.fixture(params=["stream-k", "grid"])
+def impl(request):
+    """Attention schedule, chosen when the slice is created: stream-K (the
+    default for batches up to the work-list limit) or the grid form that
+    larger batches take (EMA_CREATE_ATTN_GRID forces it)."""
     return request.param
 
 
@@ -89,7 +83,7 @@ def test_attention_shapes_and_ragged_lengths(ema, impl, hq, hkv, bs, dtype):
     print(f"attn {impl} hq={hq} hkv={hkv} bs={bs} {dtype}", flush=True)
     cfg = synth.KVConfig("grid", 1, hq, hkv, 128, dtype, bs, len(LENS), ("uniform", 0, 0), 0.4,
                          31 + bs)
-    w = Workload(cfg, lens=LENS, staging_slots=1)
+    w = Workload(cfg, lens=LENS, staging_slots=1, attn_grid=impl == "grid")
     try:
         st = w.oracle_mirror()
         w.prefetch(0)
@@ -114,7 +108,7 @@ def test_long_sequences_many_splits(ema, impl, hq, hkv, bs, dtype, lens):
     print(f"long {impl} hq={hq} hkv={hkv} bs={bs} {dtype}", flush=True)
     cfg = synth.KVConfig("long", 1, hq, hkv, 128, dtype, bs, len(lens), ("uniform", 0, 0), 0.5,
                          77 + bs)
-    w = Workload(cfg, lens=lens, staging_slots=1)
+    w = Workload(cfg, lens=lens, staging_slots=1, attn_grid=impl == "grid")
     try:
         st = w.oracle_mirror()
         w.prefetch(0)
@@ -140,7 +134,7 @@ def test_calls_with_different_cuts_on_one_handle(ema, impl):
     rng = np.random.default_rng(313)
     lens_a = rng.integers(200, 6000, 24)
     cfg = synth.KVConfig("rearm", 1, 8, 1, 128, "bf16", 32, 24, ("uniform", 0, 0), 0.5, 313)
-    w = Workload(cfg, lens=lens_a.tolist(), staging_slots=1)
+    w = Workload(cfg, lens=lens_a.tolist(), staging_slots=1, attn_grid=impl == "grid")
     try:
         st = w.oracle_mirror()
         w.prefetch(0)
@@ -169,7 +163,7 @@ def test_wide_batch_takes_the_long_chunk_path(ema, impl):
     lens = rng.integers(1, 3000, 32).tolist()
     lens[:4] = [0, 1, 512, 513]
     cfg = synth.KVConfig("wide", 1, 32, 8, 128, "bf16", 16, 32, ("uniform", 0, 0), 0.3, 91)
-    w = Workload(cfg, lens=lens, staging_slots=1)
+    w = Workload(cfg, lens=lens, staging_slots=1, attn_grid=impl == "grid")
     try:
         st = w.oracle_mirror()
         w.prefetch(0)
@@ -198,7 +192,7 @@ def test_many_short_sequences(ema, impl, batch, hi, hkv, hq):
     rng = np.random.default_rng(batch)
     lens = rng.integers(0, hi + 1, batch).tolist()
     cfg = synth.KVConfig("short", 1, hq, hkv, 128, "f16", 16, batch, ("uniform", 0, 0), 0.4, 93)
-    w = Workload(cfg, lens=lens, staging_slots=1)
+    w = Workload(cfg, lens=lens, staging_slots=1, attn_grid=impl == "grid")
     try:
         st = w.oracle_mirror()
         w.prefetch(0)
@@ -351,5 +345,56 @@ def test_70b_tp8_share_layer_sampled(ema):
     try:
         assert w.lens.max() > 4096                      # long tails exercise many splits
         sampled_parity(ema, w, 0, 6, np.random.default_rng(2))
+    finally:
+        w.close()
+
+
+def _ordered16(bits):
+    """16-bit float patterns as integers that step by one per ulp (+0 == -0)."""
+    b = np.asarray(bits, np.int64)
+    mag = b & 0x7FFF
+    return np.where(b & 0x8000, -mag, mag)
+
+
+@pytest.mark.parametrize("hq,hkv,bs,dtype,out16", [
+    (32, 8, 16, "bf16", "bf16"), (8, 1, 32, "bf16", "bf16"), (8, 8, 16, "f16", "f16"),
+    (16, 4, 128, "bf16", "f16"),
+])
+def test_16bit_output_is_the_fp32_result_rounded_to_nearest_even(ema, impl, hq, hkv, bs, dtype,
+                                                                 out16):
+    """out_dtype bf16 / fp16: every element is the fp32 output of the same call
+    rounded to nearest even (bit for bit), and within one ulp of the float64
+    oracle rounded the same way wherever the element is at least 1/64 of its
+    row's largest magnitude (below that, the fp32 result's own error, about
+    1e-6 of the row maximum, can exceed an fp16 ulp); normwise within 2e-3
+    plus the rounding bound everywhere."""
+    print(f"out16 {impl} hq={hq} hkv={hkv} bs={bs} {dtype} -> {out16}", flush=True)
+    cfg = synth.KVConfig("out16", 1, hq, hkv, 128, dtype, bs, len(LENS), ("uniform", 0, 0), 0.4,
+                         55 + bs)
+    w = Workload(cfg, lens=LENS, staging_slots=1, attn_grid=impl == "grid")
+    try:
+        st = w.oracle_mirror()
+        w.prefetch(0)
+        st.prefetch(w.pf_src[0], w.pf_dst[0])
+        o32 = w.new_out()
+        tdt = {"bf16": torch.bfloat16, "f16": torch.float16}[out16]
+        o16 = torch.full(o32.shape, float("nan"), dtype=tdt, device="cuda")
+        w.attention(0, o32)
+        ema.paged_decode_attention(w.h, w.q, w.attn_dev[0], w.lens_dev, o16)
+        torch.cuda.synchronize()
+        assert ema.slice_device_errors(w.h) == 0
+        got16 = o16.view(torch.int16).cpu().numpy().view(np.uint16)
+        got32 = o32.cpu().numpy()
+        assert np.array_equal(got16, synth.round_to_16bit(got32, out16))
+        ref = oracle_attention(w, st, 0)
+        ref16 = synth.round_to_16bit(ref.astype(np.float32), out16)
+        rowmax = np.abs(ref).max(axis=-1, keepdims=True)
+        big = np.abs(ref) >= rowmax / 64
+        ulps = np.abs(_ordered16(got16) - _ordered16(ref16))
+        assert ulps[big].max(initial=0) <= 1, ulps[big].max(initial=0)
+        as_f = o16.float().cpu().numpy()
+        u = 2.0 ** -8 if out16 == "bf16" else 2.0 ** -11
+        assert rel_err(as_f, ref) <= TOL + u
+        assert np.all(as_f[0] == 0.0)
     finally:
         w.close()
