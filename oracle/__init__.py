@@ -14,6 +14,11 @@ A plain, slow, obviously correct restatement of what the hot path computes:
 * ``invariants``: the properties the paper fixes (exactly-once ownership,
   static-dynamic symmetry after reclaim) plus conservation and the logical
   view of every block.
+* ``slab``: the slab allocator of section 4.2.1 (slabs uniform across layers,
+  one user each, freed slabs returned, reclaim of the slab with the fewest
+  active requests) with the layer-major, slab-major and layer-group-major
+  placements of sections 4.2.1-4.2.3 and the run structure of a layer-group
+  swap.
 * ``sched``: placement of slice units across GPU pairs by Greedy-Least-Loaded
   (section 5.2, Appendix C) and the cap after bursty preemptions (section 5.3).
 
@@ -38,6 +43,8 @@ from .attention import paged_decode_attention, contiguous_decode_attention
 from .invariants import (InvariantError, check_ownership, check_conservation, check_sd_symmetry,
                          logical_view)
 from .sched import SchedOracle
+from .slab import (SlabSliceOracle, LAYER_MAJOR, SLAB_MAJOR, GROUP_MAJOR, BORROWED,
+                   check_slab_tags, check_slab_sd_symmetry)
 
 __all__ = [
     "LAYOUT_ATTN", "LAYOUT_NHD", "block_bytes", "decode_block", "encode_block", "convert_block",
@@ -45,4 +52,6 @@ __all__ = [
     "ERR_INVAL", "ERR_NOMEM", "ERR_OWNER", "paged_decode_attention",
     "contiguous_decode_attention", "check_ownership", "check_conservation",
     "check_sd_symmetry", "logical_view", "InvariantError", "SchedOracle",
+    "SlabSliceOracle", "LAYER_MAJOR", "SLAB_MAJOR", "GROUP_MAJOR", "BORROWED", "check_slab_tags",
+    "check_slab_sd_symmetry",
 ]
