@@ -318,6 +318,30 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
                                void* stream);
 
 /*
+ * paged_decode_attention_noalloc -- for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same computation, arguments and result as
+ * ema_paged_decode_attention, always in the stream-K form, with its partials
+ * and combine records in a fixed per-GPU workspace (a file-scope device array
+ * of about 8.9 MB, held by each GPU the library runs on until the process
+ * ends) instead of the handle's. The call allocates nothing, on the device or
+ * on the host, and never reads device arrays back (on a checked handle it
+ * validates nothing on the host; kernels still skip and count invalid ids).
+ * All calls on one GPU share that workspace: calls that may overlap on one
+ * GPU (different streams, or concurrent host threads) race on it and must be
+ * ordered by the caller. Nothing in it needs clearing: each call writes every
+ * record it reads.
+ * Limits: batch <= 4096 (2048 at 16 query heads per KV head),
+ * batch * num_kv_heads <= 32768, at most 512 compute units; beyond them the
+ * call returns INVAL and does nothing. Other errors as for
+ * ema_paged_decode_attention.
+ */
+int ema_paged_decode_attention_noalloc(ema_slice_t h, const void* q, const int32_t* block_table,
+                                       const int32_t* seq_lens, int32_t batch,
+                                       int32_t num_q_heads, int32_t max_blocks, float scale,
+                                       void* out, int32_t out_dtype, void* stream);
+
+/*
  * Synchronizes the device, then reads and clears the number of ids the
  * kernels skipped as out of range since the last call (0 when all were valid).
  */

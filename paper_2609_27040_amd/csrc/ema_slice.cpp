@@ -50,6 +50,7 @@ struct ema_slice {
   float* d_gpart = nullptr;         // grid form: split-K partials (grows)
   size_t gpart_cap = 0;             // floats
   bool attn_grid = false;           // EMA_CREATE_ATTN_GRID: always the grid form
+  void* noalloc_ws = nullptr;       // this device's fixed workspace (not owned)
 };
 
 namespace {
@@ -268,6 +269,8 @@ int ema_slice_create(const ema_kv_shape* shape, size_t local_bytes, size_t lent_
   if (e == hipSuccess) h->part_cap = part;
   if (e == hipSuccess) e = hipMalloc(&h->d_info, info * 4);
   if (e == hipSuccess) h->info_cap = info;
+  // the no-allocation attention call's workspace on this device
+  if (e == hipSuccess) e = ema::noalloc_workspace(&h->noalloc_ws);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) return hip_fail(e, "create");   // the guard releases h
   *out = guard.release();
@@ -587,10 +590,17 @@ int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, in
   return internal_error();
 }
 
-int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* block_table,
-                               const int32_t* seq_lens, int32_t batch, int32_t num_q_heads,
-                               int32_t max_blocks, float scale, void* out, int32_t out_dtype,
-                               void* stream) try {
+}  // extern "C"
+
+namespace {
+
+// Both attention entry points. `noalloc`: stream-K only, in the fixed
+// per-device workspace, no host validation (checked mode reads arrays back)
+// and nothing that allocates.
+int attention_call(ema_slice_t h, const void* q, const int32_t* block_table,
+                   const int32_t* seq_lens, int32_t batch, int32_t num_q_heads,
+                   int32_t max_blocks, float scale, void* out, int32_t out_dtype, void* stream,
+                   bool noalloc) {
   if (!h) return fail(EMA_ERR_INVAL, "attention: NULL handle");
   const int32_t hkv = h->shape.num_kv_heads;
   if (batch < 0 || max_blocks < 0 || num_q_heads < hkv || num_q_heads % hkv != 0)
@@ -611,7 +621,7 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
   int rc = ds.enter(h);
   if (rc) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (h->checked) {
+  if (h->checked && !noalloc) {
     std::vector<int32_t> lens, tab;
     if ((rc = fetch_ints(seq_lens, batch, st, &lens)) ||
         (rc = fetch_ints(block_table, int64_t(batch) * max_blocks, st, &tab)))
@@ -632,15 +642,31 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
   // work list, else a grid of 1024-token chunks with one partial per
   // (sequence, head, chunk) in a workspace that grows on first use.
   const int64_t tiles = int64_t(batch) * hkv * ((max_tokens + 31) / 32);
-  const bool stream_k =
-      !h->attn_grid && batch <= ema::streamk_max_batch(G) && tiles < (int64_t(1) << 30);
+  const bool fits_streamk = batch <= ema::streamk_max_batch(G) && tiles < (int64_t(1) << 30);
+  if (noalloc) {
+    if (!fits_streamk)
+      return fail(EMA_ERR_INVAL, "attention_noalloc: batch above the stream-K limit (4096, or "
+                                 "2048 at 16 query heads per KV head) or max_blocks too large");
+    if (int64_t(batch) * hkv > ema::kNoAllocPairs)
+      return fail(EMA_ERR_INVAL, "attention_noalloc: batch * num_kv_heads above 32768");
+    if (ema::attn_streamk_grid() > ema::kNoAllocGrid)
+      return fail(EMA_ERR_INVAL, "attention_noalloc: more compute units than the fixed "
+                                 "workspace holds (512)");
+    if (!h->noalloc_ws) return fail(EMA_ERR_INVAL, "attention_noalloc: no fixed workspace");
+  }
+  const bool stream_k = noalloc || (!h->attn_grid && fits_streamk);
   const int32_t chunk = ema::kMfmaGridChunk;
   const int32_t n_split = int32_t(std::max<int64_t>(1, (max_tokens + chunk - 1) / chunk));
   if (!stream_k && n_split > 65535) return fail(EMA_ERR_INVAL, "attention: max_blocks too large");
   ema::AttnArgs a;
   float* part = nullptr;
   size_t part_rows = 0;
-  if (stream_k) {
+  if (noalloc) {
+    part_rows = size_t(2) * ema::attn_streamk_grid() * G;
+    part = static_cast<float*>(h->noalloc_ws);
+    a.info = reinterpret_cast<int32_t*>(static_cast<char*>(h->noalloc_ws) +
+                                        ema::kNoAllocPartFloats * 4);
+  } else if (stream_k) {
     part_rows = size_t(2) * ema::attn_streamk_grid() * G;
     part = h->d_part;
     a.info = h->d_info;
@@ -678,6 +704,28 @@ int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* bloc
   a.scale_log2 = sc * 1.4426950408889634f;
   HIP_TRY(ema::launch_paged_attention_mfma(a, st), "attention launch");
   return EMA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ema_paged_decode_attention(ema_slice_t h, const void* q, const int32_t* block_table,
+                               const int32_t* seq_lens, int32_t batch, int32_t num_q_heads,
+                               int32_t max_blocks, float scale, void* out, int32_t out_dtype,
+                               void* stream) try {
+  return attention_call(h, q, block_table, seq_lens, batch, num_q_heads, max_blocks, scale, out,
+                        out_dtype, stream, false);
+} catch (...) {
+  return internal_error();
+}
+
+int ema_paged_decode_attention_noalloc(ema_slice_t h, const void* q, const int32_t* block_table,
+                                       const int32_t* seq_lens, int32_t batch,
+                                       int32_t num_q_heads, int32_t max_blocks, float scale,
+                                       void* out, int32_t out_dtype, void* stream) try {
+  return attention_call(h, q, block_table, seq_lens, batch, num_q_heads, max_blocks, scale, out,
+                        out_dtype, stream, true);
 } catch (...) {
   return internal_error();
 }

@@ -93,6 +93,20 @@ constexpr int kMaxGroup = 16;          // query heads per KV head
 // workgroup, each kMaxGroup x (kHeadDim + 2) floats at most.
 int attn_streamk_grid();
 
+// Fixed attention workspace for callers that cannot allocate: a file-scope
+// device array (one per GPU, held until the process ends) with partial slots
+// for up to kNoAllocGrid stream-K workgroups at kMaxGroup query heads per KV
+// head, followed by combine records for kNoAllocPairs (sequence, KV head)
+// pairs. Every call writes each record it reads, so nothing in it needs
+// clearing; calls that overlap on one GPU race on it.
+constexpr int kNoAllocGrid = 512;
+constexpr int kNoAllocPairs = 32768;
+constexpr size_t kNoAllocPartFloats = size_t(2) * kNoAllocGrid * kMaxGroup * (kHeadDim + 2);
+constexpr size_t kNoAllocBytes = kNoAllocPartFloats * 4 + size_t(kNoAllocPairs) * 3 * 4;
+// Device address of that array on the current device (looked up once per
+// device with hipGetSymbolAddress, then cached).
+hipError_t noalloc_workspace(void** ptr);
+
 // Matrix-core kernel: stream-K when stream_k is set, else the grid form with
 // chunk == kMfmaGridChunk.
 hipError_t launch_paged_attention_mfma(const AttnArgs& a, hipStream_t stream);

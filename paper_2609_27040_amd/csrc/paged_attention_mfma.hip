@@ -37,6 +37,8 @@
 
 #include <algorithm>
 #include <cmath>
+#include <mutex>
+#include <unordered_map>
 
 namespace ema {
 namespace {
@@ -800,6 +802,30 @@ int attn_streamk_grid() {
     return std::min(cus, kMaxStreamGrid);
   }();
   return grid;
+}
+
+// The fixed workspace of the no-allocation entry point. Host code never uses
+// this name as an address: it takes the per-device address from
+// noalloc_workspace().
+__device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+hipError_t noalloc_workspace(void** ptr) {
+  static std::mutex mu;
+  static std::unordered_map<int, void*> addr;   // device -> address of `scratch` there
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = addr.find(dev);
+  if (it == addr.end()) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    it = addr.emplace(dev, p).first;
+  }
+  *ptr = it->second;
+  return hipSuccess;
 }
 
 hipError_t launch_paged_attention_mfma(const AttnArgs& a, hipStream_t stream) {

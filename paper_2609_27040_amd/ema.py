@@ -74,6 +74,8 @@ def _load():
         "ema_kv_append": [P, P, P, P, P, I32, I32, P],
         "ema_slice_reclaim": [P, I32, P, I64, P, ctypes.POINTER(ReclaimResult), P, I32, P, P, I32],
         "ema_paged_decode_attention": [P, P, P, P, I32, I32, I32, ctypes.c_float, P, I32, P],
+        "ema_paged_decode_attention_noalloc": [P, P, P, P, I32, I32, I32, ctypes.c_float, P, I32,
+                                               P],
         "ema_slice_device_errors": [P, ctypes.POINTER(I32)],
         "ema_sched_create": [I32, I32, I64, ctypes.POINTER(P)],
         "ema_sched_destroy": [P],
@@ -302,10 +304,7 @@ def slice_reclaim(h, n_blocks, canon_tables=None, stream=None, caps=None):
             "moves": np.stack([msrc[:m], mdst[:m]], axis=1).astype(np.int64)}
 
 
-def paged_decode_attention(h, q, block_table, seq_lens, out, scale=0.0, stream=None):
-    """q [B][Hq][D] (16-bit), block_table int32 [B][max_blocks], seq_lens int32
-    [B], out [B][Hq][D] of float32, float16 or bfloat16 (the output type is
-    the tensor's): device tensors."""
+def _attention_call(fn, h, q, block_table, seq_lens, out, scale, stream):
     import torch
     B, Hq = int(q.shape[0]), int(q.shape[1])
     max_blocks = int(block_table.shape[1]) if block_table.dim() == 2 else 0
@@ -317,9 +316,23 @@ def paged_decode_attention(h, q, block_table, seq_lens, out, scale=0.0, stream=N
         block_table = _i32_dev(block_table, "block_table", B * max_blocks)
         seq_lens = _i32_dev(seq_lens, "seq_lens", B)
         out = _dev(out, "out", tuple(out_types), B * Hq * 128)
-    _check(_lib.ema_paged_decode_attention(h, _ptr(q), _ptr(block_table), _ptr(seq_lens), B, Hq,
-                                           max_blocks, float(scale), _ptr(out),
-                                           out_types[out.dtype], _stream(stream)))
+    _check(fn(h, _ptr(q), _ptr(block_table), _ptr(seq_lens), B, Hq, max_blocks, float(scale),
+              _ptr(out), out_types[out.dtype], _stream(stream)))
+
+
+def paged_decode_attention(h, q, block_table, seq_lens, out, scale=0.0, stream=None):
+    """q [B][Hq][D] (16-bit), block_table int32 [B][max_blocks], seq_lens int32
+    [B], out [B][Hq][D] of float32, float16 or bfloat16 (the output type is
+    the tensor's): device tensors."""
+    _attention_call(_lib.ema_paged_decode_attention, h, q, block_table, seq_lens, out, scale,
+                    stream)
+
+
+def paged_decode_attention_noalloc(h, q, block_table, seq_lens, out, scale=0.0, stream=None):
+    """The same as paged_decode_attention, in the library's fixed per-GPU
+    workspace: for callers that cannot allocate (see the C header)."""
+    _attention_call(_lib.ema_paged_decode_attention_noalloc, h, q, block_table, seq_lens, out,
+                    scale, stream)
 
 
 def slice_device_errors(h):

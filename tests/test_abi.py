@@ -61,6 +61,7 @@ def test_every_entry_point_rejects_a_null_handle():
         "ema_kv_append": (z, z, z, z, z, 0, 0, z),
         "ema_slice_reclaim": (z, 0, z, 0, z, z, z, 0, z, z, 0),
         "ema_paged_decode_attention": (z, z, z, z, 0, 0, 0, 0.0, z, 2, z),
+        "ema_paged_decode_attention_noalloc": (z, z, z, z, 0, 0, 0, 0.0, z, 2, z),
         "ema_slice_device_errors": (z, z),
         "ema_sched_destroy": (z,),
         "ema_sched_create": (2, 1, 0, z),
