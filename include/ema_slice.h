@@ -348,6 +348,132 @@ int ema_paged_decode_attention_noalloc(ema_slice_t h, const void* q, const int32
 int ema_slice_device_errors(ema_slice_t h, int32_t* count);
 
 /*
+ * ---- Slab management of the slice (sections 4.2.1-4.2.3) ----
+ *
+ * A slab is `slab_blocks` (S) block positions, the same positions in every
+ * one of `layers` (L) layers, so one slab spans L*S slice slots; a slab
+ * belongs to one user at a time: the lender, nobody (lent, free) or the
+ * borrower. A borrowed slab's positions each hold one logical block of one
+ * sequence, in all L layers at once, or are free. Placement of (slab i,
+ * layer l, position p) among the slice slots, n slabs, k = group:
+ *   EMA_SLAB_LAYER_MAJOR  (l*n + i)*S + p                  (section 4.2.1)
+ *   EMA_SLAB_SLAB_MAJOR   (i*L + l)*S + p                  (section 4.2.2)
+ *   EMA_SLAB_GROUP_MAJOR  ((l/k*n + i)*k + l%k)*S + p      (section 4.2.3)
+ * In slab mode the slice's blocks are allocated, freed and reclaimed only by
+ * the ema_slab_* calls (ema_slice_alloc_blocks on the slice pool,
+ * ema_slice_free_blocks of slice ids and ema_slice_reclaim return INVAL);
+ * ema_slice_lend lends slabs (the lowest-indexed of the lender's); the local
+ * pool, migrate, prefetch, write-back, append and attention work as before,
+ * a slab position's owner being the owner of its L slots.
+ */
+#define EMA_SLAB_LAYER_MAJOR 0
+#define EMA_SLAB_SLAB_MAJOR 1
+#define EMA_SLAB_GROUP_MAJOR 2
+#define EMA_BORROWED (-4)   /* slab tag: the borrower's */
+
+typedef struct {
+  int32_t layers;        /* L: layers of the cache, every slab spans all of them */
+  int32_t slab_blocks;   /* S: block positions per slab */
+  int32_t group;         /* k: layers per layer group (divides L) */
+  int32_t layout;        /* EMA_SLAB_* */
+} ema_slab_cfg;
+
+typedef struct {
+  int32_t n_slabs;       /* floor(n_slice / (L*S)); slots past them stay the lender's */
+  int32_t layers, slab_blocks, group, layout;
+  int32_t borrowed;      /* slabs the borrower holds */
+} ema_slab_info;
+
+typedef struct {
+  int32_t reclaimed;     /* slabs returned to the lender: min(n, slabs lent) */
+  int32_t n_victims;     /* sequences preempted */
+  int32_t released;      /* blocks those sequences held (local and slab) */
+} ema_slab_reclaim_result;
+
+/*
+ * slab_init -- manage an untouched slice (every slot lent and free, as after
+ * create) in slabs: all slabs FREE (lent, unused). Device: allocates the
+ * lists the layer-group swaps copy from (4 bytes per slice slot, device and
+ * pinned host). Errors: INVAL (already in slabs, slice touched, layers, S or
+ * group < 1, group not dividing layers, bad layout, no whole slab), HIP.
+ */
+int ema_slab_init(ema_slice_t h, const ema_slab_cfg* cfg);
+
+/* Slab shape and state; slab_tag[n_slabs] (EMA_LENDER, EMA_FREE or
+ * EMA_BORROWED) and pos_owner[n_slabs*S] (owner or EMA_FREE) may be NULL. */
+int ema_slab_get_info(ema_slice_t h, ema_slab_info* out, int32_t* slab_tag, int32_t* pos_owner);
+
+/*
+ * slab_alloc -- a task that exhausts its memory requests more slabs (section
+ * 4.2.1). One position per owners[i] (a sequence, >= 0), in order: the lowest
+ * free position of the borrowed slabs (slab index order), and when those are
+ * full the lowest-indexed free slab is borrowed. out_pos[n] (host) gets the
+ * positions i*S + p. All or nothing. Errors: INVAL, NOMEM.
+ */
+int ema_slab_alloc(ema_slice_t h, int32_t n, const int32_t* owners, int32_t* out_pos);
+
+/*
+ * slab_free -- positions back to free; a borrowed slab left without a block
+ * returns to the slice for either user (section 4.2.1). Errors: INVAL (range,
+ * duplicate), OWNER (a free position).
+ */
+int ema_slab_free(ema_slice_t h, const int32_t* pos, int32_t n);
+
+/*
+ * The unified ids of layer `layer`'s blocks at slab positions pos[n] (host):
+ * with staging_first < 0 the slice blocks; otherwise the blocks the swap of
+ * that layer's group puts them in, in the staging image that starts at local
+ * block staging_first (their slabs must be borrowed). Errors: INVAL.
+ */
+int ema_slab_block_ids(ema_slice_t h, const int32_t* pos, int32_t n, int32_t layer,
+                       int32_t staging_first, int32_t* out_ids);
+
+/*
+ * The swap of layer group `group` as runs (host arrays of cap entries; any
+ * may be NULL): every borrowed slab's blocks of the group's layers, used and
+ * unused positions alike, into a staging image at staging_first that keeps
+ * the slice layout's order -- (j*m + r)*S + p for layer-major, (r*k + j)*S + p
+ * otherwise (r: rank among the m borrowed slabs, j: layer within the group).
+ * Runs are maximal ranges contiguous on both sides, in staging order, so their
+ * sizes are S..mS (layer-major), kS (slab-major), kS..mkS (layer-group-major).
+ * *n_runs receives the total even past cap. Errors: INVAL.
+ */
+int ema_slab_group_runs(ema_slice_t h, int32_t group, int32_t staging_first, int32_t* src_first,
+                        int32_t* dst_first, int32_t* run_blocks, int32_t cap, int32_t* n_runs);
+
+/*
+ * slab_prefetch_group -- at a layer-group boundary the group's swap is issued
+ * (section 4.2.2): local blocks staging_first + t <- the t-th block of the
+ * group's swap (as above), m*k*S blocks, all of which must be EMA_STAGING
+ * local blocks. engine EMA_ENGINE_KERNEL: the gather kernel over a source list
+ * kept on the device (rebuilt, with one upload, only when the set of borrowed
+ * slabs changed); EMA_ENGINE_DMA: one copy-engine transfer per run (slice in
+ * EMA_LAYOUT_ATTN only). Async on `stream`. Errors: INVAL, HIP.
+ */
+int ema_slab_prefetch_group(ema_slice_t h, int32_t group, int32_t staging_first, int32_t engine,
+                            void* stream);
+
+/*
+ * slab_reclaim -- the lender takes back n_slabs slabs (section 4.2.1: the
+ * allocator selects the borrower's slab with the fewest active requests;
+ * section 4.1: reclamation preempts requests, each releasing its whole
+ * dependency chain). For each slab: the highest-indexed free slab if there is
+ * one; else the borrowed slab with the fewest distinct sequences (ties: the
+ * highest index), whose sequences are preempted in ascending order -- every
+ * block each holds, local or in any slab, becomes free, slabs left empty
+ * return to the slice -- and the slab goes to the lender. Every entry of
+ * canon_tables (device int32 [n_entries], rewritten in place on `stream`)
+ * naming a released block becomes -1; no data moves. slabs[slabs_cap] and
+ * victims[victims_cap] (host, may be NULL) get the slabs taken and the
+ * preempted sequences in order. In host-only mode canon_tables must be NULL.
+ * The rewrite list uses the handle's plan upload area (see the conventions).
+ * Errors: INVAL, HIP (after the bookkeeping took effect, as for reclaim).
+ */
+int ema_slab_reclaim(ema_slice_t h, int32_t n_slabs, int32_t* canon_tables, int64_t n_entries,
+                     void* stream, ema_slab_reclaim_result* result, int32_t* slabs,
+                     int32_t slabs_cap, int32_t* victims, int32_t victims_cap);
+
+/*
  * Slice scheduling across GPUs (section 5.2, Appendix C) and bursty
  * preemption control (section 5.3) -- host policy, no device work.
  *

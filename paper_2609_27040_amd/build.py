@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIBDIR = os.path.join(PKG, "lib")
 LIB = os.path.join(LIBDIR, "libema_slice.so")
 
-SOURCES = ["slice_book.cpp", "ema_slice.cpp", "slice_sched.cpp", "block_copy.hip",
+SOURCES = ["slice_book.cpp", "slab_book.cpp", "ema_slice.cpp", "slice_sched.cpp", "block_copy.hip",
            "paged_attention_mfma.hip", "attn_combine.hip"]
 
 ARCH = "gfx950"

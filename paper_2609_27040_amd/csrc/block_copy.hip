@@ -95,7 +95,7 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
                                                          const int32_t* __restrict__ src_ids,
                                                          const int32_t* __restrict__ dst_ids,
                                                          int32_t n, int32_t* err_count,
-                                                         TableRewrite rw) {
+                                                         TableRewrite rw, int32_t dst_base) {
   extern __shared__ __attribute__((aligned(16))) uint16_t lds_tile[];
   if (int(blockIdx.x) < rw.n_groups) {
     rewrite_tables(rw, blockIdx.x);
@@ -109,7 +109,7 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
   const int32_t i = int32_t(unit / upb);
   const int k = int(unit - int64_t(i) * upb);
   const int32_t s = src_ids[i];
-  const int32_t d = dst_ids[i];
+  const int32_t d = dst_ids ? dst_ids[i] : dst_base + i;
   const int32_t n_total = pv.n_local + pv.n_slice;
   if (s < 0 || s >= n_total || d < 0 || d >= n_total) {
     if (k == 0 && lane == 0) atomicAdd(err_count, 1);
@@ -262,7 +262,8 @@ __global__ __launch_bounds__(256) void block_copy_same_kernel(PoolView pv,
                                                               const int32_t* __restrict__ src_ids,
                                                               const int32_t* __restrict__ dst_ids,
                                                               int32_t n, int32_t* err_count,
-                                                              TableRewrite rw) {
+                                                              TableRewrite rw,
+                                                              int32_t dst_base) {
   if (int(blockIdx.x) < rw.n_groups) {
     rewrite_tables(rw, blockIdx.x);
     return;
@@ -275,7 +276,7 @@ __global__ __launch_bounds__(256) void block_copy_same_kernel(PoolView pv,
   const int32_t i = int32_t(piece / ppb);
   const int k = int(piece - int64_t(i) * ppb);
   const int32_t s = src_ids[i];
-  const int32_t d = dst_ids[i];
+  const int32_t d = dst_ids ? dst_ids[i] : dst_base + i;
   const int32_t n_total = pv.n_local + pv.n_slice;
   if (s < 0 || s >= n_total || d < 0 || d >= n_total) {
     if (k == 0 && lane == 0) atomicAdd(err_count, 1);
@@ -325,7 +326,7 @@ __global__ __launch_bounds__(128) void kv_append_kernel(PoolView pv, const uint1
 
 hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32_t* dst,
                              int32_t n, int32_t* err_count, hipStream_t stream, bool runs,
-                             const TableRewrite* rw) {
+                             const TableRewrite* rw, int32_t dst_base) {
   TableRewrite rwl;
   if (rw && rw->n_entries > 0) {
     rwl = *rw;
@@ -346,12 +347,15 @@ hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32
     const int32_t m = int32_t(std::max<int64_t>(0, std::min<int64_t>(max_blocks, n - b0)));
     const int64_t grid = (int64_t(m) * upb + wg_waves - 1) / wg_waves + rwl.n_groups;
     const unsigned threads = same ? unsigned(64 * wg_waves) : 256u;
+    const int32_t* s0 = m ? src + b0 : nullptr;
+    const int32_t* d0 = m && dst ? dst + b0 : nullptr;
+    const int32_t base0 = dst ? 0 : int32_t(dst_base + b0);
     if (same)
       hipLaunchKernelGGL(block_copy_same_kernel, dim3(unsigned(grid)), dim3(threads), 0, stream,
-                         pv, src + b0, dst + b0, m, err_count, rwl);
+                         pv, s0, d0, m, err_count, rwl, base0);
     else
       hipLaunchKernelGGL(block_copy_kernel, dim3(unsigned(grid)), dim3(threads), lds, stream, pv,
-                         src + b0, dst + b0, m, err_count, rwl);
+                         s0, d0, m, err_count, rwl, base0);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     rwl.n_groups = 0;

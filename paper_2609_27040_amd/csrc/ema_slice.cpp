@@ -51,6 +51,15 @@ struct ema_slice {
   size_t gpart_cap = 0;             // floats
   bool attn_grid = false;           // EMA_CREATE_ATTN_GRID: always the grid form
   void* noalloc_ws = nullptr;       // this device's fixed workspace (not owned)
+  // slab mode: every layer group's swap sources (staging order), on the device
+  int32_t* d_slab = nullptr;
+  int32_t* h_slab = nullptr;        // pinned
+  size_t slab_cap = 0;              // ints
+  int64_t slab_built = -1;          // slab version the device lists were built for
+  int32_t slab_m = 0;               // borrowed slabs when they were built
+  hipEvent_t slab_up_ev = nullptr;  // after the last upload of the lists
+  hipEvent_t slab_use_ev = nullptr; // after the last kernel that read them
+  bool slab_up_pending = false, slab_use_pending = false;
 };
 
 namespace {
@@ -179,6 +188,10 @@ void release(ema_slice* h) {
     if (h->h_work) (void)hipHostFree(h->h_work);
     if (h->h_work_ev) (void)hipEventDestroy(h->h_work_ev);
     if (h->d_work_ev) (void)hipEventDestroy(h->d_work_ev);
+    if (h->d_slab) (void)hipFree(h->d_slab);
+    if (h->h_slab) (void)hipHostFree(h->h_slab);
+    if (h->slab_up_ev) (void)hipEventDestroy(h->slab_up_ev);
+    if (h->slab_use_ev) (void)hipEventDestroy(h->slab_use_ev);
   }
   delete h;
 }
@@ -726,6 +739,270 @@ int ema_paged_decode_attention_noalloc(ema_slice_t h, const void* q, const int32
                                        void* out, int32_t out_dtype, void* stream) try {
   return attention_call(h, q, block_table, seq_lens, batch, num_q_heads, max_blocks, scale, out,
                         out_dtype, stream, true);
+} catch (...) {
+  return internal_error();
+}
+
+// ---- slab mode ---------------------------------------------------------------
+
+int ema_slab_init(ema_slice_t h, const ema_slab_cfg* cfg) try {
+  if (!h || !cfg) return fail(EMA_ERR_INVAL, "slab_init: NULL argument");
+  ema::SlabCfg c;
+  c.layers = cfg->layers;
+  c.slab_blocks = cfg->slab_blocks;
+  c.group = cfg->group;
+  c.layout = cfg->layout;
+  if (h->host_only) {
+    std::string err;
+    const int rc = h->book.slab_init(c, &err);
+    return rc ? fail(rc, err) : EMA_OK;
+  }
+  DeviceScope ds;
+  int rc = ds.enter(h);
+  if (rc) return rc;
+  // device lists of every group's swap sources: at most every slabbed slot once
+  const size_t cap = size_t(h->book.n_slice()) + 1;
+  hipError_t e = hipSuccess;
+  if (!h->d_slab) {
+    e = hipMalloc(&h->d_slab, cap * 4);
+    if (e == hipSuccess) e = hipHostMalloc(&h->h_slab, cap * 4, hipHostMallocDefault);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&h->slab_up_ev, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&h->slab_use_ev, hipEventDisableTiming);
+    if (e != hipSuccess) return hip_fail(e, "slab_init");
+    h->slab_cap = cap;
+  }
+  std::string err;
+  rc = h->book.slab_init(c, &err);
+  return rc ? fail(rc, err) : EMA_OK;
+} catch (...) {
+  return internal_error();
+}
+
+int ema_slab_get_info(ema_slice_t h, ema_slab_info* out, int32_t* slab_tag, int32_t* pos_owner) try {
+  if (!h || !out) return fail(EMA_ERR_INVAL, "slab_info: NULL argument");
+  if (!h->book.slab_mode()) return fail(EMA_ERR_INVAL, "slab_info: the slice is not in slabs");
+  const ema::SlabCfg& c = h->book.slab_cfg();
+  out->n_slabs = h->book.n_slabs();
+  out->layers = c.layers;
+  out->slab_blocks = c.slab_blocks;
+  out->group = c.group;
+  out->layout = c.layout;
+  out->borrowed = int32_t(h->book.borrowed_slabs().size());
+  if (slab_tag) std::copy(h->book.slab_tag().begin(), h->book.slab_tag().end(), slab_tag);
+  if (pos_owner) std::copy(h->book.pos_owner().begin(), h->book.pos_owner().end(), pos_owner);
+  return EMA_OK;
+} catch (...) {
+  return internal_error();
+}
+
+int ema_slab_alloc(ema_slice_t h, int32_t n, const int32_t* owners, int32_t* out_pos) try {
+  if (!h) return fail(EMA_ERR_INVAL, "slab_alloc: NULL handle");
+  std::string err;
+  const int rc = h->book.slab_alloc(n, owners, out_pos, &err);
+  return rc ? fail(rc, err) : EMA_OK;
+} catch (...) {
+  return internal_error();
+}
+
+int ema_slab_free(ema_slice_t h, const int32_t* pos, int32_t n) try {
+  if (!h) return fail(EMA_ERR_INVAL, "slab_free: NULL handle");
+  std::string err;
+  const int rc = h->book.slab_free(pos, n, &err);
+  return rc ? fail(rc, err) : EMA_OK;
+} catch (...) {
+  return internal_error();
+}
+
+int ema_slab_block_ids(ema_slice_t h, const int32_t* pos, int32_t n, int32_t layer,
+                       int32_t staging_first, int32_t* out_ids) try {
+  if (!h) return fail(EMA_ERR_INVAL, "slab_block_ids: NULL handle");
+  if (!h->book.slab_mode()) return fail(EMA_ERR_INVAL, "slab_block_ids: the slice is not in slabs");
+  if (n < 0 || (n > 0 && (!pos || !out_ids)))
+    return fail(EMA_ERR_INVAL, "slab_block_ids: n < 0 or NULL array");
+  const ema::SlabCfg& c = h->book.slab_cfg();
+  if (layer < 0 || layer >= c.layers) return fail(EMA_ERR_INVAL, "slab_block_ids: bad layer");
+  const int32_t S = c.slab_blocks;
+  const int64_t n_pos = int64_t(h->book.n_slabs()) * S;
+  std::vector<int32_t> rank;
+  int32_t m = 0;
+  if (staging_first >= 0) {
+    rank.assign(size_t(h->book.n_slabs()), -1);
+    for (int32_t i : h->book.borrowed_slabs()) rank[i] = m++;
+  }
+  for (int32_t k = 0; k < n; ++k) {
+    if (pos[k] < 0 || pos[k] >= n_pos)
+      return fail(EMA_ERR_INVAL, "slab_block_ids: position out of range");
+    const int32_t i = pos[k] / S, p = pos[k] % S;
+    if (staging_first < 0) {
+      out_ids[k] = int32_t(h->book.n_local() + h->book.slab_slot(i, layer, p));
+    } else {
+      if (rank[i] < 0) return fail(EMA_ERR_INVAL, "slab_block_ids: position of a slab not borrowed");
+      const int64_t id = staging_first + h->book.stage_index(rank[i], m, layer % c.group, p);
+      if (id >= h->book.n_local())
+        return fail(EMA_ERR_INVAL, "slab_block_ids: staging image past the local pool");
+      out_ids[k] = int32_t(id);
+    }
+  }
+  return EMA_OK;
+} catch (...) {
+  return internal_error();
+}
+
+// Runs of group g's swap into the staging image at staging_first: maximal
+// ranges contiguous on both sides, in staging order.
+static void slab_runs(const ema_slice* h, int32_t g, int32_t staging_first,
+                      std::vector<int32_t>* rs, std::vector<int32_t>* rd, std::vector<int32_t>* rn) {
+  std::vector<int32_t> src;
+  h->book.group_sources(g, &src);
+  rs->clear();
+  rd->clear();
+  rn->clear();
+  for (size_t i = 0; i < src.size(); ++i) {
+    const int32_t d = staging_first + int32_t(i);
+    if (!rn->empty() && rs->back() + rn->back() == src[i] && rd->back() + rn->back() == d) {
+      ++rn->back();
+    } else {
+      rs->push_back(src[i]);
+      rd->push_back(d);
+      rn->push_back(1);
+    }
+  }
+}
+
+static int check_group(const ema_slice* h, int32_t g, int32_t staging_first, const char* what) {
+  if (!h->book.slab_mode())
+    return fail(EMA_ERR_INVAL, std::string(what) + ": the slice is not in slabs");
+  const ema::SlabCfg& c = h->book.slab_cfg();
+  if (g < 0 || g >= c.layers / c.group) return fail(EMA_ERR_INVAL, std::string(what) + ": bad group");
+  if (staging_first < 0) return fail(EMA_ERR_INVAL, std::string(what) + ": bad staging_first");
+  return EMA_OK;
+}
+
+int ema_slab_group_runs(ema_slice_t h, int32_t group, int32_t staging_first, int32_t* src_first,
+                        int32_t* dst_first, int32_t* run_blocks, int32_t cap,
+                        int32_t* n_runs) try {
+  if (!h || !n_runs) return fail(EMA_ERR_INVAL, "slab_group_runs: NULL argument");
+  int rc = check_group(h, group, staging_first, "slab_group_runs");
+  if (rc) return rc;
+  std::vector<int32_t> rs, rd, rn;
+  slab_runs(h, group, staging_first, &rs, &rd, &rn);
+  *n_runs = int32_t(rn.size());
+  for (int32_t i = 0; i < int32_t(rn.size()) && i < cap; ++i) {
+    if (src_first) src_first[i] = rs[i];
+    if (dst_first) dst_first[i] = rd[i];
+    if (run_blocks) run_blocks[i] = rn[i];
+  }
+  return EMA_OK;
+} catch (...) {
+  return internal_error();
+}
+
+int ema_slab_prefetch_group(ema_slice_t h, int32_t group, int32_t staging_first, int32_t engine,
+                            void* stream) try {
+  if (!h) return fail(EMA_ERR_INVAL, "slab_prefetch_group: NULL handle");
+  int rc = check_group(h, group, staging_first, "slab_prefetch_group");
+  if (rc) return rc;
+  if (engine != EMA_ENGINE_KERNEL && engine != EMA_ENGINE_DMA)
+    return fail(EMA_ERR_INVAL, "slab_prefetch_group: unknown engine");
+  if (engine == EMA_ENGINE_DMA && h->shape.slice_layout != EMA_LAYOUT_ATTN)
+    return fail(EMA_ERR_INVAL,
+                "slab_prefetch_group: the copy engines need the slice in the local layout");
+  const ema::SlabCfg& c = h->book.slab_cfg();
+  const int32_t m = int32_t(h->book.borrowed_slabs().size());
+  const int64_t count = int64_t(m) * c.group * c.slab_blocks;
+  if (staging_first + count > h->book.n_local())
+    return fail(EMA_ERR_INVAL, "slab_prefetch_group: staging image past the local pool");
+  for (int64_t i = 0; i < count; ++i)
+    if (h->book.owner(int32_t(staging_first + i)) != EMA_STAGING)
+      return fail(EMA_ERR_INVAL, "slab_prefetch_group: staging image holds a non-staging block");
+  if (h->host_only || count == 0) return EMA_OK;
+  DeviceScope ds;
+  if ((rc = ds.enter(h))) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (engine == EMA_ENGINE_DMA) {
+    std::vector<int32_t> rs, rd, rn;
+    slab_runs(h, group, staging_first, &rs, &rd, &rn);
+    const ema::PoolView pv = pool_view(h);
+    for (size_t r = 0; r < rn.size(); ++r) {
+      char* d = pv.local + int64_t(rd[r]) * h->bb;
+      const char* sp = pv.slice + (int64_t(rs[r]) - pv.n_local) * h->bb;
+      HIP_TRY(hipMemcpyAsync(d, sp, size_t(rn[r]) * h->bb, hipMemcpyDeviceToDeviceNoCU, st),
+              "slab_prefetch_group copy");
+    }
+    return EMA_OK;
+  }
+  if (h->slab_built != h->book.slab_version()) {
+    // every group's sources, rebuilt only when the set of borrowed slabs changed
+    if (size_t(m) * c.layers * c.slab_blocks > h->slab_cap)
+      return fail(EMA_ERR_INVAL, "slab_prefetch_group: lists larger than their buffer");
+    if (h->slab_up_pending) {
+      HIP_TRY(hipEventSynchronize(h->slab_up_ev), "hipEventSynchronize(slab lists)");
+      h->slab_up_pending = false;
+    }
+    if (h->slab_use_pending) HIP_TRY(hipStreamWaitEvent(st, h->slab_use_ev, 0), "hipStreamWaitEvent");
+    std::vector<int32_t> src;
+    size_t off = 0;
+    for (int32_t g = 0; g < c.layers / c.group; ++g) {
+      h->book.group_sources(g, &src);
+      std::copy(src.begin(), src.end(), h->h_slab + off);
+      off += src.size();
+    }
+    HIP_TRY(hipMemcpyAsync(h->d_slab, h->h_slab, off * 4, hipMemcpyHostToDevice, st),
+            "hipMemcpyAsync(slab lists)");
+    HIP_TRY(hipEventRecord(h->slab_up_ev, st), "hipEventRecord(slab lists)");
+    h->slab_up_pending = true;
+    h->slab_built = h->book.slab_version();
+    h->slab_m = m;
+  }
+  HIP_TRY(ema::launch_block_copy(pool_view(h), h->d_slab + size_t(group) * count, nullptr,
+                                 int32_t(count), h->d_err, st, true, nullptr, staging_first),
+          "slab_prefetch_group launch");
+  HIP_TRY(hipEventRecord(h->slab_use_ev, st), "hipEventRecord(slab prefetch)");
+  h->slab_use_pending = true;
+  return EMA_OK;
+} catch (...) {
+  return internal_error();
+}
+
+int ema_slab_reclaim(ema_slice_t h, int32_t n_slabs, int32_t* canon_tables, int64_t n_entries,
+                     void* stream, ema_slab_reclaim_result* result, int32_t* slabs,
+                     int32_t slabs_cap, int32_t* victims, int32_t victims_cap) try {
+  if (!h || !result) return fail(EMA_ERR_INVAL, "slab_reclaim: NULL handle or result");
+  if (n_slabs < 0 || n_entries < 0 || (n_entries > 0 && !canon_tables))
+    return fail(EMA_ERR_INVAL, "slab_reclaim: bad count or table pointer");
+  if (h->host_only && (canon_tables || n_entries))
+    return fail(EMA_ERR_INVAL, "slab_reclaim: host-only slices take no device tables");
+  int rc;
+  DeviceScope ds;
+  if (!h->host_only && (rc = ds.enter(h))) return rc;
+  ema::SlabReclaimPlan plan;
+  std::string err;
+  if ((rc = h->book.slab_reclaim(n_slabs, &plan, &err))) return fail(rc, err);
+  result->reclaimed = plan.reclaimed;
+  result->n_victims = int32_t(plan.victims.size());
+  result->released = int32_t(plan.released.size());
+  for (int32_t i = 0; slabs && i < int32_t(plan.slabs.size()) && i < slabs_cap; ++i)
+    slabs[i] = plan.slabs[i];
+  for (int32_t i = 0; victims && i < result->n_victims && i < victims_cap; ++i)
+    victims[i] = plan.victims[i];
+  if (h->host_only || n_entries == 0 || plan.released.empty()) return EMA_OK;
+  // every released block's table entries become -1 (no data moves: the
+  // preempted requests are dropped)
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const size_t need = plan.released.size();
+  if (need > h->h_work_cap || need > h->work_cap)
+    return fail(EMA_ERR_INVAL, "slab_reclaim: plan larger than the work buffers");
+  if ((rc = begin_upload(h, st))) return rc;
+  std::copy(plan.released.begin(), plan.released.end(), h->h_work);
+  if ((rc = upload(h, need, st))) return rc;
+  ema::TableRewrite rw;
+  rw.tables = canon_tables;
+  rw.n_entries = n_entries;
+  rw.victims = h->d_work;
+  rw.n_victims = int32_t(need);
+  HIP_TRY(ema::launch_block_copy(pool_view(h), nullptr, nullptr, 0, h->d_err, st, true, &rw),
+          "slab_reclaim rewrite");
+  return end_upload(h, st);
 } catch (...) {
   return internal_error();
 }

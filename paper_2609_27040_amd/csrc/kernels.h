@@ -42,10 +42,12 @@ constexpr int kRewriteEntries = 8192;   // table entries per rewriting workgroup
 // `runs`: the lists are mostly ascending runs of ids (reclaim moves,
 // contiguous-run prefetches) rather than scattered blocks; only the work
 // distribution depends on it. `rw` (optional): the table rewrite to run in the
-// same launch (n_groups is set by the launcher).
+// same launch (n_groups is set by the launcher). dst == nullptr: the
+// destinations are dst_base + i (a contiguous staging image).
 hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32_t* dst,
                              int32_t n, int32_t* err_count, hipStream_t stream,
-                             bool runs = false, const TableRewrite* rw = nullptr);
+                             bool runs = false, const TableRewrite* rw = nullptr,
+                             int32_t dst_base = 0);
 
 // New decode token of every sequence into its block (ATTN layout): row
 // (len-1) % bs of local block table[b][(len-1) / bs], len = seq_lens[b] > 0.

@@ -100,6 +100,10 @@ int SliceBook::alloc(int32_t pool, int32_t n, const int32_t* owners, int32_t* ou
     *err = "alloc: bad pool";
     return kErrInval;
   }
+  if (pool == 1 && slab_mode_) {
+    *err = "alloc: the slice is managed in slabs (slab_alloc)";
+    return kErrInval;
+  }
   FreeBits& fb = pool == 0 ? free_local_ : free_slice_;
   const int32_t limit = pool == 0 ? n_local_ : lim_;
   if (fb.count_below(limit) < n) {
@@ -132,6 +136,11 @@ int SliceBook::free_blocks(const int32_t* ids, int32_t n, std::string* err) {
       *err = "free: duplicate id";
       return kErrInval;
     }
+  for (int32_t i = 0; i < n; ++i)
+    if (slab_mode_ && ids[i] >= n_local_) {
+      *err = "free: the slice is managed in slabs (slab_free)";
+      return kErrInval;
+    }
   for (int32_t i = 0; i < n; ++i) {
     if (!in_range(ids[i])) {
       *err = "free: id out of range";
@@ -151,6 +160,16 @@ int SliceBook::lend(int32_t n, int32_t* added, std::string* err) {
   if (n < 0) {
     *err = "lend: n < 0";
     return kErrInval;
+  }
+  if (slab_mode_) {   // the lowest-indexed lender's slabs
+    int32_t got = 0;
+    for (int32_t i = 0; i < n_slabs_ && got < n; ++i)
+      if (slab_tag_[i] == kLender) {
+        set_slab(i, kFree);
+        ++got;
+      }
+    if (added) *added = got;
+    return kOk;
   }
   const int32_t nw = int32_t(std::min<int64_t>(n_slice_, int64_t(lim_) + n));
   const int32_t old = lim_;
@@ -237,6 +256,10 @@ int SliceBook::check_writeback(const int32_t* src, const int32_t* dst, int32_t n
 int SliceBook::reclaim(int32_t n, ReclaimPlan* p, std::string* err) {
   if (n < 0) {
     *err = "reclaim: n < 0";
+    return kErrInval;
+  }
+  if (slab_mode_) {
+    *err = "reclaim: the slice is managed in slabs (slab_reclaim)";
     return kErrInval;
   }
   *p = ReclaimPlan();

@@ -21,6 +21,8 @@ OK, ERR_INVAL, ERR_NOMEM, ERR_OWNER, ERR_HIP = 0, -1, -2, -3, -4
 F16, BF16, F32 = 0, 1, 2
 LAYOUT_ATTN, LAYOUT_NHD = 0, 1
 ENGINE_KERNEL, ENGINE_DMA = 0, 1
+SLAB_LAYER_MAJOR, SLAB_SLAB_MAJOR, SLAB_GROUP_MAJOR = 0, 1, 2
+BORROWED = -4
 POOL_LOCAL, POOL_SLICE = 0, 1
 FREE, STAGING, LENDER = -1, -2, -3
 CREATE_HOST_ONLY, CREATE_CHECKED, CREATE_ATTN_GRID = 1, 2, 4
@@ -53,6 +55,22 @@ class ReclaimResult(ctypes.Structure):
                 ("lim", ctypes.c_int32)]
 
 
+class SlabCfg(ctypes.Structure):
+    _fields_ = [("layers", ctypes.c_int32), ("slab_blocks", ctypes.c_int32),
+                ("group", ctypes.c_int32), ("layout", ctypes.c_int32)]
+
+
+class SlabInfo(ctypes.Structure):
+    _fields_ = [("n_slabs", ctypes.c_int32), ("layers", ctypes.c_int32),
+                ("slab_blocks", ctypes.c_int32), ("group", ctypes.c_int32),
+                ("layout", ctypes.c_int32), ("borrowed", ctypes.c_int32)]
+
+
+class SlabReclaimResult(ctypes.Structure):
+    _fields_ = [("reclaimed", ctypes.c_int32), ("n_victims", ctypes.c_int32),
+                ("released", ctypes.c_int32)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
@@ -77,6 +95,14 @@ def _load():
         "ema_paged_decode_attention_noalloc": [P, P, P, P, I32, I32, I32, ctypes.c_float, P, I32,
                                                P],
         "ema_slice_device_errors": [P, ctypes.POINTER(I32)],
+        "ema_slab_init": [P, ctypes.POINTER(SlabCfg)],
+        "ema_slab_get_info": [P, ctypes.POINTER(SlabInfo), P, P],
+        "ema_slab_alloc": [P, I32, P, P],
+        "ema_slab_free": [P, P, I32],
+        "ema_slab_block_ids": [P, P, I32, I32, I32, P],
+        "ema_slab_group_runs": [P, I32, I32, P, P, P, I32, ctypes.POINTER(I32)],
+        "ema_slab_prefetch_group": [P, I32, I32, I32, P],
+        "ema_slab_reclaim": [P, I32, P, I64, P, ctypes.POINTER(SlabReclaimResult), P, I32, P, I32],
         "ema_sched_create": [I32, I32, I64, ctypes.POINTER(P)],
         "ema_sched_destroy": [P],
         "ema_sched_place": [P, I32, I32, I32, I64, P, ctypes.POINTER(I32)],
@@ -339,6 +365,84 @@ def slice_device_errors(h):
     c = ctypes.c_int32()
     _check(_lib.ema_slice_device_errors(h, ctypes.byref(c)))
     return c.value
+
+
+# ---- slab management of the slice --------------------------------------------------
+
+def slab_init(h, layers, slab_blocks, group, layout=SLAB_GROUP_MAJOR):
+    cfg = SlabCfg(int(layers), int(slab_blocks), int(group), int(layout))
+    _check(_lib.ema_slab_init(h, ctypes.byref(cfg)))
+
+
+def slab_get_info(h):
+    """Shape and state: dict with n_slabs, layers, slab_blocks, group, layout,
+    borrowed, slab_tag (int32 [n_slabs]) and pos_owner (int32 [n_slabs * S])."""
+    info = SlabInfo()
+    _check(_lib.ema_slab_get_info(h, ctypes.byref(info), None, None))
+    tag = np.empty(info.n_slabs, dtype=np.int32)
+    own = np.empty(info.n_slabs * info.slab_blocks, dtype=np.int32)
+    _check(_lib.ema_slab_get_info(h, ctypes.byref(info), tag.ctypes.data, own.ctypes.data))
+    d = {k: getattr(info, k) for k, _ in SlabInfo._fields_}
+    d["slab_tag"], d["pos_owner"] = tag, own
+    return d
+
+
+def slab_alloc(h, owners):
+    owners = _i32_host(owners)
+    out = np.empty(len(owners), dtype=np.int32)
+    _check(_lib.ema_slab_alloc(h, len(owners), owners.ctypes.data, out.ctypes.data))
+    return out
+
+
+def slab_free(h, positions):
+    positions = _i32_host(positions)
+    _check(_lib.ema_slab_free(h, positions.ctypes.data, len(positions)))
+
+
+def slab_block_ids(h, positions, layer, staging_first=-1):
+    """Unified ids of `layer`'s blocks at the positions (slice blocks, or
+    their staged copies when staging_first >= 0)."""
+    positions = _i32_host(positions)
+    out = np.empty(len(positions), dtype=np.int32)
+    _check(_lib.ema_slab_block_ids(h, positions.ctypes.data, len(positions), int(layer),
+                                   int(staging_first), out.ctypes.data))
+    return out
+
+
+def slab_group_runs(h, group, staging_first):
+    """(src_first, dst_first, run_blocks) int32 arrays of the group's swap."""
+    n = ctypes.c_int32()
+    _check(_lib.ema_slab_group_runs(h, int(group), int(staging_first), None, None, None, 0,
+                                    ctypes.byref(n)))
+    a, b, c = (np.empty(max(n.value, 1), dtype=np.int32) for _ in range(3))
+    _check(_lib.ema_slab_group_runs(h, int(group), int(staging_first), a.ctypes.data,
+                                    b.ctypes.data, c.ctypes.data, n.value, ctypes.byref(n)))
+    return a[:n.value], b[:n.value], c[:n.value]
+
+
+def slab_prefetch_group(h, group, staging_first, engine=ENGINE_KERNEL, stream=None):
+    _check(_lib.ema_slab_prefetch_group(h, int(group), int(staging_first), int(engine),
+                                        None if _host_only(h) else _stream(stream)))
+
+
+def slab_reclaim(h, n_slabs, canon_tables=None, stream=None):
+    """Returns reclaimed, n_victims, released counts plus the slabs taken and
+    the victims (lists)."""
+    info = slab_get_info(h)
+    res = SlabReclaimResult()
+    slabs = np.empty(max(info["n_slabs"], 1), dtype=np.int32)
+    cap = int(info["n_slabs"] * info["slab_blocks"] + 1)
+    victims = np.empty(cap, dtype=np.int32)
+    host_only = _host_only(h)
+    if canon_tables is not None and not host_only:
+        canon_tables = _i32_dev(canon_tables, "canon_tables")
+    n_entries = 0 if canon_tables is None else canon_tables.numel()
+    _check(_lib.ema_slab_reclaim(h, int(n_slabs), _ptr(canon_tables), n_entries,
+                                 None if host_only else _stream(stream), ctypes.byref(res),
+                                 slabs.ctypes.data, len(slabs), victims.ctypes.data, cap))
+    return {"reclaimed": res.reclaimed, "released": res.released,
+            "slabs": slabs[:res.reclaimed].tolist(),
+            "victims": victims[:min(res.n_victims, cap)].tolist()}
 
 
 # ---- slice scheduling across GPUs (host policy) -------------------------------------

@@ -159,6 +159,8 @@ class BurstyTrace:
                 for k in ("reclaimed", "moved", "written_back", "lim"):
                     assert r[k] == mr[k], f"reclaim {k}: {r[k]} != oracle {mr[k]}"
                 assert list(r["victims"]) == list(mr["victims"]), "reclaim victims differ"
+                assert np.array_equal(mv, np.asarray(mr["moves"], np.int64).reshape(-1, 2)), \
+                    "reclaim moves differ from the oracle's"
                 assert np.array_equal(t, self.mtables), "reclaim: tables differ from the oracle's"
             self.log.append(("reclaim", n, r["moved"], r["written_back"], list(r["victims"])))
             for v in r["victims"]:

@@ -34,7 +34,7 @@ def stress_blocks(cfg, bs):
 
 class StressRun:
     def __init__(self, bs, n_blocks=None, seqs=1024, slice_layout=ema.LAYOUT_ATTN,
-                 cfg=synth.STRESS, samples=256):
+                 cfg=synth.STRESS, samples=256, mirror=False):
         N = stress_blocks(cfg, bs) if n_blocks is None else int(n_blocks)
         per_seq = max(1, N // seqs)
         tok = per_seq * bs
@@ -48,6 +48,18 @@ class StressRun:
         self.s = torch.cuda.Stream()
         self.timer = BlockedTimer()
         self.ns_per_mover = 50.0        # host planning estimate, refined as reclaims run
+        # an oracle without block data replaying every allocation, free, lend,
+        # migration and reclaim: plans and tables are compared with it
+        self.mirror = None
+        if mirror:
+            import oracle
+            st = oracle.SliceOracle(w.hkv, w.D, w.bs, c.dtype, slice_layout,
+                                    w.local_view.shape[0] * w.bb, w.slice_view.shape[0] * w.bb,
+                                    with_data=False)
+            for pool, owners in w.alloc_log:
+                st.alloc_blocks(pool, owners)
+            self.mirror = st
+            self.mtables = w.tables.copy()
 
     # ---- helpers ---------------------------------------------------------------------
     def _rows(self, ids):
@@ -101,6 +113,8 @@ class StressRun:
 
     def free_staging(self):
         ema.slice_free_blocks(self.w.h, self.w.staging.ravel())
+        if self.mirror is not None:
+            self.mirror.free_blocks(self.w.staging.ravel())
 
     def reclaim_sweep(self, fractions=FRACTIONS):
         w = self.w
@@ -128,19 +142,34 @@ class StressRun:
                 tables[:, v, :] = -1
             dev = w.tables_dev.cpu().numpy().reshape(tables.shape)
             tables_ok = np.array_equal(dev, tables.astype(np.int32))
+            oracle_ok = None
+            if self.mirror is not None:
+                mr = self.mirror.reclaim(n, self.mtables)
+                oracle_ok = (np.array_equal(mv, np.asarray(mr["moves"], np.int64).reshape(-1, 2))
+                             and list(r["victims"]) == list(mr["victims"])
+                             and r["lim"] == mr["lim"] and r["written_back"] == mr["written_back"]
+                             and np.array_equal(tables, self.mtables))
             after_ids = remap[pick]
             exact = self._same_content(before, pick, self._rows(after_ids), after_ids)
             nbytes = 2 * r["moved"] * w.bb + 8 * w.tables_dev.numel()
             rec = {"frac": p, "n": n, "moved": r["moved"], "written_back": r["written_back"],
                    "victims": len(r["victims"]), "ms": ms, "host_plan_ms": host_ms,
                    "device_only": covered, "GBps": nbytes / (ms / 1e3) / 1e9,
-                   "tables_ok": tables_ok, "exact": exact}
+                   "tables_ok": tables_ok, "exact": exact, "oracle_ok": oracle_ok}
             # lend the slots again and move the blocks back into the slice
             ema.slice_lend(w.h, n)
+            if self.mirror is not None:
+                self.mirror.lend(n)
             if len(mv):
                 pos = np.argwhere(np.isin(tables, mv[:, 1]))
                 cur = tables[pos[:, 0], pos[:, 1], pos[:, 2]]
                 back = ema.slice_alloc_blocks(w.h, ema.POOL_SLICE, pos[:, 1]).astype(np.int64)
+                if self.mirror is not None:
+                    mback = self.mirror.alloc_blocks(ema.POOL_SLICE, pos[:, 1])
+                    rec["oracle_ok"] = rec["oracle_ok"] and np.array_equal(back, mback)
+                    self.mirror.migrate(cur, back)
+                    self.mirror.free_blocks(cur)
+                    self.mtables[pos[:, 0], pos[:, 1], pos[:, 2]] = back
                 src_t = torch.as_tensor(cur.astype(np.int32), device="cuda")
                 dst_t = torch.as_tensor(back.astype(np.int32), device="cuda")
                 _, mms, _, _ = self.timer.time(

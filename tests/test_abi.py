@@ -63,6 +63,14 @@ def test_every_entry_point_rejects_a_null_handle():
         "ema_paged_decode_attention": (z, z, z, z, 0, 0, 0, 0.0, z, 2, z),
         "ema_paged_decode_attention_noalloc": (z, z, z, z, 0, 0, 0, 0.0, z, 2, z),
         "ema_slice_device_errors": (z, z),
+        "ema_slab_init": (z, z),
+        "ema_slab_get_info": (z, z, z, z),
+        "ema_slab_alloc": (z, 0, z, z),
+        "ema_slab_free": (z, z, 0),
+        "ema_slab_block_ids": (z, z, 0, 0, 0, z),
+        "ema_slab_group_runs": (z, 0, 0, z, z, z, 0, z),
+        "ema_slab_prefetch_group": (z, 0, 0, 0, z),
+        "ema_slab_reclaim": (z, 0, z, 0, z, z, z, 0, z, 0),
         "ema_sched_destroy": (z,),
         "ema_sched_create": (2, 1, 0, z),
         "ema_sched_place": (z, 0, 0, 0, 0, z, z),

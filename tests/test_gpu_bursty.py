@@ -10,11 +10,14 @@ pools are compared byte for byte (staging blocks aside: the oracle does not
 prefetch) and the last layer's attention output against the oracle's float64
 attention over the canonical tables.
 
-Full size (the 8B-shaped cache, 32 layers, batch 64, 200 steps): every step
-the device-rewritten tables against the host's own application of the reclaim
-plan and the ownership invariants; at the end the content of every logical
-block of the sequences never preempted (checksums taken before the trace) and
-the attention output of sampled sequences against the oracle.
+Full size (the 8B-shaped cache, 32 layers, batch 64, 200 steps): an oracle
+without block data replays every allocation, free, lend, migration and
+reclaim, and every step the owners, lent limit, reclaim moves, victims and
+rewritten tables are compared with it (the device-rewritten tables also
+against the host's own application of the plan), plus the ownership
+invariants; at the end the content of every logical block of the sequences
+never preempted (checksums taken before the trace) and the attention output
+of sampled sequences against the oracle.
 """
 import numpy as np
 import pytest
@@ -97,7 +100,7 @@ def test_bursty_trace_scaled_matches_oracle(ema, layout, local_frac, mode, group
 def test_bursty_trace_full_size(ema):
     from bursty import BurstyTrace
     print("bursty full size", flush=True)
-    tr = BurstyTrace(synth.BURSTY, fill="device")
+    tr = BurstyTrace(synth.BURSTY, fill="device", mirror="owners")
     try:
         fp0 = tr.fingerprints()
         ms = []

@@ -276,3 +276,51 @@ def test_captured_step_replays_match_eager(ema):
     finally:
         w.close()
 
+
+
+@pytest.mark.parametrize("bs", [16, 32, 64, 128, 256])
+@pytest.mark.parametrize("hkv", [1, 8])
+def test_relayout_both_directions_every_block_size(ema, bs, hkv):
+    """Token-major slice: write-back (local layout -> slice layout), migration
+    into the slice and migration out of it at every block size, both whole
+    pools byte-equal to the oracle. The relayout units change shape with the
+    block size (16-, 32- and 64-token units), so each size is its own case."""
+    print(f"relayout bs={bs} hkv={hkv}", flush=True)
+    bb = oracle.block_bytes(hkv, D, bs)
+    n_l, n_s = 14, 12
+    h = ema.slice_create(hkv, D, bs, "f16", 1, n_l * bb, n_s * bb)
+    st = oracle.SliceOracle(hkv, D, bs, "f16", 1, n_l * bb, n_s * bb)
+    rng = np.random.default_rng(bs * 10 + hkv)
+    st.local[:] = rng.integers(0, 256, st.local.shape, dtype=np.uint8)
+    st.slice[:] = rng.integers(0, 256, st.slice.shape, dtype=np.uint8)
+    lv, sv = ema.pool_view(h, ema.POOL_LOCAL), ema.pool_view(h, ema.POOL_SLICE)
+    lv.copy_(torch.from_numpy(st.local))
+    sv.copy_(torch.from_numpy(st.slice))
+    try:
+        def both(call, *args):
+            getattr(ema, call)(h, *[i32(a) for a in args])
+            getattr(st, call.replace("slice_", ""))(*args)
+        # write-back: 4 staged local blocks -> 4 slice blocks (scattered order)
+        sdst = ema.slice_alloc_blocks(h, ema.POOL_SLICE, [0, 1, 2, 3])
+        st.alloc_blocks(oracle.SLICE, [0, 1, 2, 3])
+        stg = ema.slice_alloc_blocks(h, ema.POOL_LOCAL, [ema.STAGING] * 4)
+        st.alloc_blocks(oracle.LOCAL, [oracle.STAGING] * 4)
+        both("slice_writeback", stg[[2, 0, 3, 1]], sdst)
+        # migrate into the slice: 3 local blocks of sequence 5
+        lsrc = ema.slice_alloc_blocks(h, ema.POOL_LOCAL, [5, 5, 5])
+        st.alloc_blocks(oracle.LOCAL, [5, 5, 5])
+        sdst2 = ema.slice_alloc_blocks(h, ema.POOL_SLICE, [5, 5, 5])
+        st.alloc_blocks(oracle.SLICE, [5, 5, 5])
+        both("slice_migrate", lsrc, sdst2[::-1])
+        # migrate out of the slice: sequence 1's and 2's slice blocks -> local
+        ldst = ema.slice_alloc_blocks(h, ema.POOL_LOCAL, [1, 2])
+        st.alloc_blocks(oracle.LOCAL, [1, 2])
+        both("slice_migrate", sdst[[1, 2]], ldst)
+        torch.cuda.synchronize()
+        assert ema.slice_device_errors(h) == 0
+        assert np.array_equal(lv.cpu().numpy(), st.local)
+        assert np.array_equal(sv.cpu().numpy(), st.slice)
+    finally:
+        lv = sv = None
+        torch.cuda.synchronize()
+        ema.slice_destroy(h)

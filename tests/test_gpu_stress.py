@@ -4,7 +4,9 @@ with write-back and a migration back after each.
 
 Checked: sampled blocks bit for bit after every copy (layout-independently for
 a token-major slice), the device-rewritten tables against the host's
-application of each reclaim plan, and the reclaim counts (the local pool has
+application of each reclaim plan, each plan (moves, victims, lent limit) and
+the rewritten tables against an oracle without block data that replays every
+allocation, free, lend, migration and reclaim, and the reclaim counts (the local pool has
 room for every borrowed block, so every mover is written back and nothing is
 preempted; the slice is full, so every slot of the returned range moves).
 """
@@ -27,7 +29,7 @@ def ema():
 def test_stress_prefetch_and_reclaim_sweep(ema, bs, layout, n_blocks):
     from stress import StressRun
     print(f"stress bs={bs} layout={layout} n_blocks={n_blocks}", flush=True)
-    run = StressRun(bs, n_blocks=n_blocks, slice_layout=layout)
+    run = StressRun(bs, n_blocks=n_blocks, slice_layout=layout, mirror=True)
     try:
         pf = run.prefetch_all(reps=1)
         assert pf["exact"], "prefetch: sampled blocks differ"
@@ -36,6 +38,7 @@ def test_stress_prefetch_and_reclaim_sweep(ema, bs, layout, n_blocks):
         sweep = run.reclaim_sweep()
         for r in sweep:
             assert r["tables_ok"], f"{r['frac']}: device tables differ"
+            assert r["oracle_ok"], f"{r['frac']}: plan or tables differ from the oracle's"
             assert r["exact"], f"{r['frac']}: sampled written-back blocks differ"
             assert r["moved"] == r["n"] == r["written_back"] and r["victims"] == 0, r
             assert ema.slice_get_info(run.w.h)["lim"] == lim0     # lent back after each
