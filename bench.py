@@ -46,9 +46,8 @@ import time
 import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
-for p in (ROOT, os.path.join(ROOT, "tests")):
-    if p not in sys.path:
-        sys.path.insert(0, p)
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 # Sources whose code runs in one attention call; a counter record is valid for
@@ -90,6 +89,12 @@ def parse():
     ap.add_argument("--reclaim-reps", type=int, default=4)
     ap.add_argument("--symmetry-reps", type=int, default=6,
                     help="A/B pairs of the staged vs all-local attention passes (0: skip)")
+    ap.add_argument("--no-legs", action="store_true",
+                    help="skip the other workloads' compact legs reported beside the headline "
+                         "(70B TP-8 share step, stress prefetch, token-major slice, slab sweep, "
+                         "copy ceilings)")
+    ap.add_argument("--legs", default="c3,stress,nhd,slabs,ceiling",
+                    help="which compact legs to run (comma-separated)")
     return ap.parse_args()
 
 
@@ -173,8 +178,13 @@ def cpu_baseline(w, seconds):
     """The oracle timed on this host's cores on a bounded sample: float64
     attention of layer 0 for whole sequences, and block prefetch copies."""
     import oracle
-    from harness import read_blocks
+    import torch
     from threadpoolctl import threadpool_limits
+
+    def read_blocks(view, ids):
+        ids = np.asarray(ids, dtype=np.int64)
+        data = view[torch.from_numpy(ids).to(view.device)].cpu().numpy()
+        return {int(u): data[i] for i, u in enumerate(ids)}
 
     rng = np.random.default_rng(0)
     order = rng.permutation(w.B)[:16]
@@ -299,7 +309,7 @@ def alt_mode_steps(w, out, mode, args, attn_b):
     """The same steps in the other schedule, timed the same way (reported beside
     the headline, not part of it)."""
     import torch
-    from harness import StepRunner
+    from paper_2609_27040_amd.step import StepRunner
     log(f"{mode} steps for comparison")
     runner = StepRunner(w, mode)
     for _ in range(args.warmup):
@@ -322,7 +332,7 @@ def graph_steps(w, out, runner, args):
     roofline stays with the eager steps). The replay's output must equal an
     eager step's bit for bit."""
     import torch
-    from harness import capture_step
+    from paper_2609_27040_amd.step import capture_step
     log("graph-captured steps for comparison")
     runner.run(out)
     torch.cuda.synchronize()
@@ -346,13 +356,17 @@ def graph_steps(w, out, runner, args):
 
 
 def hbm_context(torch, gib=2, reps=5):
-    """A plain torch device-to-device copy (read + write counted) on this GPU
-    in the same run, as context for the fractions of 8 TB/s."""
+    """A plain torch device-to-device copy (read + write counted) and a plain
+    read (a float32 sum of 2 GiB of bf16) on this GPU in the same run, as
+    context for the fractions of 8 TB/s."""
     n = (gib << 30) // 2
     x = torch.randn(n, device="cuda", dtype=torch.float32).to(torch.bfloat16)
     y = torch.empty_like(x)
     res = {}
-    for name, fn, nbytes in (("torch_copy_GBps", lambda: y.copy_(x), 4 * n),):
+    acc = torch.empty((), device="cuda", dtype=torch.float32)
+    for name, fn, nbytes in (("torch_copy_GBps", lambda: y.copy_(x), 4 * n),
+                             ("torch_read_GBps", lambda: torch.sum(x, 0, dtype=torch.float32,
+                                                                   out=acc), 2 * n)):
         fn()
         torch.cuda.synchronize()
         ts = []
@@ -375,7 +389,7 @@ def reclaim_phase(w, s, reps, ema, torch):
     so the events bracket only device work: upload of the plan, block copies,
     table rewrite. ``host_plan_ms`` is the call's host time; ``device_only``
     says whether the copy was indeed still running when the call returned."""
-    from harness import BlockedTimer
+    from paper_2609_27040_amd.step import BlockedTimer
     timer = BlockedTimer()
     res = []
     for _ in range(reps):
@@ -399,7 +413,7 @@ def bursty_main(args):
     latency distribution (one JSON line)."""
     import torch
     import synth
-    from bursty import BurstyTrace
+    from workloads.bursty import BurstyTrace
 
     torch.cuda.set_device(0)
     cfg = synth.BURSTY
@@ -457,7 +471,7 @@ def stress_main(args):
     to local), each followed by a migration back; prints one JSON line."""
     import torch
     import synth
-    from stress import StressRun, stress_blocks
+    from workloads.stress import StressRun, stress_blocks
 
     torch.cuda.set_device(0)
     cfg = synth.STRESS
@@ -517,7 +531,7 @@ def slab_main(args):
     block-size-16 pool (8 GiB, 60 % slice) as contiguous runs of 1 to 400
     blocks, by the gather kernel and by the copy engines; one JSON line."""
     import torch
-    from stress import run_sweep
+    from workloads.stress import run_sweep
 
     torch.cuda.set_device(0)
     log("slab sweep")
@@ -536,6 +550,170 @@ def slab_main(args):
         log(f"run {r['run_blocks']:4d} blocks: kernel {r['kernel']['GBps']:.0f} GB/s, "
             f"copy engines {r['dma']['GBps']:.0f} GB/s (end to end {r['dma']['wall_GBps']:.0f})")
     print(json.dumps(res))
+
+
+def measure_steps(w, runner, steps, warmup, timed_layers=2):
+    """Times `steps` steps after `warmup`: whole-step wall time between two
+    device synchronisations, attention per call and prefetch per group from
+    event pairs (one layer group per step, rotating)."""
+    import torch
+    from types import SimpleNamespace
+    a = SimpleNamespace(timed_layers=timed_layers)
+    out = w.new_out()
+    for _ in range(warmup):
+        runner.run(out)
+    torch.cuda.synchronize()
+    timers = [step_timers(runner, a, k) for k in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(steps):
+        runner.run(out, timers[k])
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / steps
+    at_ms, at_calls = attention_samples(timers, w)
+    pf_b = [2 * len(src) * w.bb for src in w.pf_src_grp]
+    pf_ms = np.array([e0.elapsed_time(e1) for tm in timers for e0, e1 in tm["pf"].values()])
+    pf_timed_b = float(sum(pf_b[k] for tm in timers for k in tm["pf"]))
+    attn_b = attention_bytes(w)
+    at_mean_s = float(at_ms.mean()) / 1e3
+    attn_gbps = attn_b / at_mean_s / 1e9
+    pf_gbps = pf_timed_b / (pf_ms.sum() / 1e3) / 1e9 if len(pf_ms) else 0.0
+    step_bytes = attn_b * w.L + float(np.sum(pf_b))
+    return out, {
+        "ms_per_step": ms_step, "tokens_per_s": w.B / (ms_step / 1e3),
+        "attention": {"bytes_per_launch": attn_b, "timed_calls": int(at_calls),
+                      "mean_us": at_mean_s * 1e6,
+                      "tokens_per_s_attention_only": w.B / (w.L * at_mean_s),
+                      "p10_us": pct(at_ms, 10) * 1e3, "p90_us": pct(at_ms, 90) * 1e3,
+                      "GBps": attn_gbps, "frac": attn_gbps / HBM_PEAK_GBPS},
+        "prefetch": {"bytes_per_step": float(np.sum(pf_b)),
+                     "mean_us": float(pf_ms.mean()) * 1e3 if len(pf_ms) else 0.0,
+                     "GBps": pf_gbps, "frac": pf_gbps / HBM_PEAK_GBPS},
+        "step": {"bytes": step_bytes, "GBps": step_bytes / (ms_step / 1e3) / 1e9,
+                 "frac": step_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBPS}}
+
+
+def roofline_obj(achieved, traffic_rec, kernel, key="bytes_per_call"):
+    r = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+         "frac": achieved / HBM_PEAK_GBPS, "traffic": None, "kernel": kernel}
+    if traffic_rec is not None:
+        r["traffic"] = traffic_rec.get(key)
+        r["traffic_source"] = traffic_rec.get("note", "counter summary")
+    return r
+
+
+def step_leg(cfg, steps, warmup, group=4, slice_layout=0, counters=None, sources=ATTN_SOURCES,
+             roof="attention"):
+    """One workload's one-stream step (compact: no other schedule, graph,
+    symmetry or reclaim phase). The roofline is the attention entry point's,
+    or with roof="prefetch" the group prefetch copy's."""
+    import torch
+    from paper_2609_27040_amd import ema
+    from paper_2609_27040_amd.step import StepRunner
+    from workloads.synthetic import Workload
+    log(f"leg: {cfg.name}, slice layout {slice_layout}")
+    w = Workload(cfg, fill="device", staging_slots=2 * group, group=group,
+                 slice_layout=slice_layout)
+    try:
+        runner = StepRunner(w, "serial")
+        _, rec = measure_steps(w, runner, steps, warmup)
+        if ema.slice_device_errors(w.h):
+            raise RuntimeError(f"{cfg.name}: kernels skipped invalid ids")
+    finally:
+        w.close()
+        torch.cuda.empty_cache()
+    log(f"  {rec['ms_per_step']:.3f} ms/step, attention {rec['attention']['mean_us']:.1f} us "
+        f"({rec['attention']['GBps']:.0f} GB/s), prefetch {rec['prefetch']['GBps']:.0f} GB/s")
+    crec = counter_record(counters, sources) if counters else None
+    if roof == "attention":
+        rec["roofline"] = roofline_obj(rec["attention"]["GBps"], crec,
+                                       "paged_decode_attention (attn_mfma_streamk + "
+                                       "attn_combine_streamk)")
+    else:
+        rec["roofline"] = roofline_obj(rec["prefetch"]["GBps"], crec,
+                                       "block_copy_kernel (group prefetch, token-major slice "
+                                       "re-laid into the local layout)", key="bytes_per_launch")
+    rec["config"] = {"workload": cfg.name, "layers": w.L, "batch": w.B, "q_heads": cfg.q_heads,
+                     "kv_heads": cfg.kv_heads, "block_size": cfg.block_size,
+                     "lens": list(cfg.lens), "slice_frac": cfg.slice_frac, "layer_group": group,
+                     "slice_layout": "token-major" if slice_layout else "local"}
+    rec["steps"], rec["warmup"] = steps, warmup
+    return rec
+
+
+def stress_leg(block_sizes=(16, 64, 256)):
+    """Prefetch of every slice block of the large-block stress pools (one
+    call per block size) and one reclaim of 5 % of the lent slots with
+    write-back, sampled blocks compared bit for bit."""
+    import torch
+    from workloads.stress import StressRun
+    out = {}
+    for bs in block_sizes:
+        log(f"leg: stress block size {bs}")
+        run = StressRun(bs)
+        try:
+            pf = run.prefetch_all(reps=3)
+            run.free_staging()
+            rc = run.reclaim_sweep(fractions=(0.05,))[0]
+        finally:
+            run.close()
+            torch.cuda.empty_cache()
+        if not (pf["exact"] and rc["exact"] and rc["tables_ok"]):
+            raise RuntimeError(f"stress block size {bs}: sampled blocks or tables differ")
+        log(f"  prefetch {pf['GBps']:.0f} GB/s, reclaim of 5 % {rc['GBps']:.0f} GB/s")
+        out[str(bs)] = {"blocks": run.N, "block_bytes": run.w.bb, "prefetch_GBps": pf["GBps"],
+                        "prefetch_ms": pf["ms"], "reclaim_5pct_GBps": rc["GBps"],
+                        "reclaim_5pct_ms": rc["ms"], "reclaim_moved": rc["moved"]}
+    best = max(out, key=lambda k: out[k]["prefetch_GBps"])
+    crec = counter_record("block_copy_stress_counters.md", COPY_SOURCES)
+    traffic = None
+    if crec is not None and best in crec.get("per_block_size", {}):
+        traffic = crec["per_block_size"][best]["bytes_per_launch"]
+    roof = roofline_obj(out[best]["prefetch_GBps"], None,
+                        f"block_copy_same_kernel (prefetch of every slice block, block size {best})")
+    roof["traffic"] = traffic
+    if crec is not None:
+        roof["traffic_source"] = crec.get("note", "counter summary")
+    return {"roofline": roof, "per_block_size": out}
+
+
+def slab_leg(points, steps=3, warmup=1):
+    """The 8B-shaped step on a slab-managed slice with interleaved free slabs
+    (workloads.slabs), per (slab size, layer group, engine)."""
+    import torch
+    import synth
+    from paper_2609_27040_amd import ema
+    from workloads.slabs import run_point, slab_cache
+    rows = []
+    for S, k, eng in points:
+        log(f"leg: slab step S={S} group={k} engine={eng}")
+        c = slab_cache(synth.LLAMA8B, S, k, engine=eng)
+        try:
+            rows.append(run_point(c, steps=steps, warmup=warmup))
+            if ema.slice_device_errors(c.h):
+                raise RuntimeError("slab step: kernels skipped invalid ids")
+        finally:
+            c.close()
+            torch.cuda.empty_cache()
+        r = rows[-1]
+        log(f"  {r['ms_per_step']:.2f} ms/step, swap {r['swap_GBps']:.0f} GB/s, "
+            f"{r['runs_per_step']} runs of {r['mean_run_KiB']:.0f} KiB")
+    return rows
+
+
+def ceiling_leg():
+    """What this GPU's HBM gives the library's own copy on long contiguous
+    runs (the kernel engine of the run prefetch, 400-block runs of 64 KiB),
+    beside torch's plain copy and plain read, in the same process."""
+    import torch
+    from workloads.stress import run_sweep
+    log("leg: copy ceilings")
+    rows = run_sweep(run_blocks=(400,), engines=("kernel",))
+    res = {"library_copy_contiguous_GBps": rows[0]["kernel"]["GBps"],
+           "library_copy_run_blocks": 400}
+    res.update(hbm_context(torch))
+    log("  " + ", ".join(f"{k} {v:.0f}" for k, v in res.items()))
+    return res
 
 
 def main():
@@ -558,7 +736,8 @@ def main():
         return
     import torch
     import synth
-    from harness import StepRunner, Workload
+    from paper_2609_27040_amd.step import StepRunner
+    from workloads.synthetic import Workload
     from paper_2609_27040_amd import ema
 
     torch.cuda.set_device(0)
@@ -577,34 +756,15 @@ def main():
     s1 = runner.s1
     out = w.new_out()
     attn_b = attention_bytes(w)
-    pf_b = [2 * len(src) * w.bb for src in w.pf_src_grp]      # per layer group
 
     log(f"warmup {args.warmup}, timed {args.steps} steps ({args.mode})")
-    for _ in range(args.warmup):
-        runner.run(out)
-    torch.cuda.synchronize()
-    # every timing event costs device time, so each step times one layer
-    # group (rotating over the steps) and the rest run without events
-    timers = [step_timers(runner, args, k) for k in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        runner.run(out, timers[k])
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_step = (t1 - t0) * 1e3 / args.steps
+    out, core = measure_steps(w, runner, args.steps, args.warmup, timed_layers=args.timed_layers)
+    ms_step = core["ms_per_step"]
     errs = ema.slice_device_errors(w.h)
     if errs:
         raise RuntimeError(f"kernels skipped {errs} invalid ids")
-
-    at_ms, at_calls = attention_samples(timers, w)
-    pf_ms = np.array([e0.elapsed_time(e1) for tm in timers for e0, e1 in tm["pf"].values()])
-    pf_timed_b = float(sum(pf_b[k] for tm in timers for k in tm["pf"]))
-    at_mean_s = float(at_ms.mean()) / 1e3
-    attn_gbps = attn_b / at_mean_s / 1e9
-    pf_gbps = pf_timed_b / (pf_ms.sum() / 1e3) / 1e9
-    step_bytes = attn_b * L + float(np.sum(pf_b))
-    log(f"{ms_step:.3f} ms/step, attention {at_mean_s * 1e6:.1f} us/layer")
+    attn_gbps = core["attention"]["GBps"]
+    log(f"{ms_step:.3f} ms/step, attention {core['attention']['mean_us']:.1f} us/layer")
 
     alt = None
     if not args.no_alt_mode:
@@ -642,18 +802,11 @@ def main():
         "roofline": {"bound": "hbm", "achieved": attn_gbps, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": attn_gbps / HBM_PEAK_GBPS, "traffic": traffic,
                      "kernel": "paged_decode_attention (attn_mfma_streamk + attn_combine_streamk)"},
-        "attention": {"bytes_per_launch": attn_b, "timed_calls": int(at_calls),
-                      "timing": ("one event pair per call" if args.append else
-                                 f"one event pair around each timed group's {w.group} "
-                                 "consecutive calls"),
-                      "mean_us": at_mean_s * 1e6,
-                      "tokens_per_s_attention_only": B / (L * at_mean_s),
-                      "p10_us": pct(at_ms, 10) * 1e3, "p90_us": pct(at_ms, 90) * 1e3,
-                      "GBps": attn_gbps, "frac": attn_gbps / HBM_PEAK_GBPS},
-        "prefetch": {"bytes_per_step": float(np.sum(pf_b)), "mean_us": float(pf_ms.mean()) * 1e3,
-                     "GBps": pf_gbps, "frac": pf_gbps / HBM_PEAK_GBPS},
-        "step": {"bytes": step_bytes, "GBps": step_bytes / (ms_step / 1e3) / 1e9,
-                 "frac": step_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBPS},
+        "attention": dict(core["attention"], timing=(
+            "one event pair per call" if args.append else
+            f"one event pair around each timed group's {w.group} consecutive calls")),
+        "prefetch": core["prefetch"],
+        "step": core["step"],
     }
     if rec is not None:
         res["roofline"]["traffic_source"] = rec.get("note", "counter summary")
@@ -680,9 +833,44 @@ def main():
     if errs:
         raise RuntimeError(f"kernels skipped {errs} invalid ids")
     w.close()
-    if not args.no_cpu_baseline:                  # the full default run only
+    del w, runner, out
+    torch.cuda.empty_cache()
+    if not args.no_legs and cfg.name == "llama3-8b-kv":
+        res["legs"] = run_legs(args)
+    elif not args.no_cpu_baseline:
         res["hbm_context"] = hbm_context(torch)
     print(json.dumps(res))
+
+
+def run_legs(args):
+    """The other workloads, compact, beside the headline (each with its own
+    roofline object): the 70B TP-8 share's step, the stress pools' prefetch and
+    reclaim, the 8B step with a token-major slice (the relayout copy), the
+    slab step sweep, and the copy ceilings of this GPU."""
+    import synth
+    want = set(args.legs.split(","))
+    legs = {}
+    t0 = time.perf_counter()
+    if "c3" in want:
+        legs["llama-70b-tp8-share"] = step_leg(
+            synth.L70B_TP8, steps=10, warmup=2,
+            counters="paged_attention_llama-70b-tp8-share_counters.md")
+    if "stress" in want:
+        legs["stress"] = stress_leg()
+    if "nhd" in want:
+        legs["llama3-8b-kv-token-major-slice"] = step_leg(
+            synth.LLAMA8B, steps=10, warmup=2, slice_layout=1,
+            counters="block_copy_token_major_prefetch_counters.md", sources=COPY_SOURCES,
+            roof="prefetch")
+    if "slabs" in want:
+        from paper_2609_27040_amd import ema
+        pts = [(S, k, ema.ENGINE_KERNEL) for S in (1, 10, 100) for k in (1, 2, 4)]
+        pts += [(S, 4, ema.ENGINE_DMA) for S in (1, 10, 100)]
+        legs["slab-sweep"] = slab_leg(pts)
+    if "ceiling" in want:
+        legs["copy-ceilings"] = ceiling_leg()
+    legs["seconds"] = time.perf_counter() - t0
+    return legs
 
 
 if __name__ == "__main__":

@@ -10,7 +10,7 @@ import torch
 
 import oracle
 import synth
-from harness import Workload, rel_err, read_blocks
+from harness import Workload, oracle_mirror, read_blocks, rel_err
 
 pytestmark = pytest.mark.gpu
 TOL = 2e-3
@@ -44,7 +44,7 @@ def test_tiny_config_end_to_end(ema, layout):
     print(f"tiny layout={layout}", flush=True)
     w = Workload(synth.TINY, slice_layout=layout, staging_slots=1, extra_local=200)
     try:
-        st = w.oracle_mirror()
+        st = oracle_mirror(w)
         w.prefetch(0)
         st.prefetch(w.pf_src[0], w.pf_dst[0])
         out = w.new_out()
@@ -85,7 +85,7 @@ def test_attention_shapes_and_ragged_lengths(ema, impl, hq, hkv, bs, dtype):
                          31 + bs)
     w = Workload(cfg, lens=LENS, staging_slots=1, attn_grid=impl == "grid")
     try:
-        st = w.oracle_mirror()
+        st = oracle_mirror(w)
         w.prefetch(0)
         st.prefetch(w.pf_src[0], w.pf_dst[0])
         out = w.new_out()
@@ -110,7 +110,7 @@ def test_long_sequences_many_splits(ema, impl, hq, hkv, bs, dtype, lens):
                          77 + bs)
     w = Workload(cfg, lens=lens, staging_slots=1, attn_grid=impl == "grid")
     try:
-        st = w.oracle_mirror()
+        st = oracle_mirror(w)
         w.prefetch(0)
         st.prefetch(w.pf_src[0], w.pf_dst[0])
         out = w.new_out()
@@ -136,7 +136,7 @@ def test_calls_with_different_cuts_on_one_handle(ema, impl):
     cfg = synth.KVConfig("rearm", 1, 8, 1, 128, "bf16", 32, 24, ("uniform", 0, 0), 0.5, 313)
     w = Workload(cfg, lens=lens_a.tolist(), staging_slots=1, attn_grid=impl == "grid")
     try:
-        st = w.oracle_mirror()
+        st = oracle_mirror(w)
         w.prefetch(0)
         st.prefetch(w.pf_src[0], w.pf_dst[0])
         cases = [(24, lens_a), (24, lens_a // 3), (10, lens_a[:10]), (24, lens_a[::-1] % 700),
@@ -165,7 +165,7 @@ def test_wide_batch_takes_the_long_chunk_path(ema, impl):
     cfg = synth.KVConfig("wide", 1, 32, 8, 128, "bf16", 16, 32, ("uniform", 0, 0), 0.3, 91)
     w = Workload(cfg, lens=lens, staging_slots=1, attn_grid=impl == "grid")
     try:
-        st = w.oracle_mirror()
+        st = oracle_mirror(w)
         w.prefetch(0)
         st.prefetch(w.pf_src[0], w.pf_dst[0])
         out = w.new_out()
@@ -194,7 +194,7 @@ def test_many_short_sequences(ema, impl, batch, hi, hkv, hq):
     cfg = synth.KVConfig("short", 1, hq, hkv, 128, "f16", 16, batch, ("uniform", 0, 0), 0.4, 93)
     w = Workload(cfg, lens=lens, staging_slots=1, attn_grid=impl == "grid")
     try:
-        st = w.oracle_mirror()
+        st = oracle_mirror(w)
         w.prefetch(0)
         st.prefetch(w.pf_src[0], w.pf_dst[0])
         out = w.new_out()
@@ -231,7 +231,7 @@ def test_random_configurations(ema, seed):
                          2000 + seed)
     w = Workload(cfg, lens=lens.tolist(), slice_layout=layout, staging_slots=1)
     try:
-        st = w.oracle_mirror()
+        st = oracle_mirror(w)
         w.prefetch(0)
         st.prefetch(w.pf_src[0], w.pf_dst[0])
         out = w.new_out()
@@ -373,7 +373,7 @@ def test_16bit_output_is_the_fp32_result_rounded_to_nearest_even(ema, impl, hq, 
                          55 + bs)
     w = Workload(cfg, lens=LENS, staging_slots=1, attn_grid=impl == "grid")
     try:
-        st = w.oracle_mirror()
+        st = oracle_mirror(w)
         w.prefetch(0)
         st.prefetch(w.pf_src[0], w.pf_dst[0])
         o32 = w.new_out()

@@ -25,7 +25,7 @@ import torch
 
 import oracle
 import synth
-from harness import rel_err, read_blocks
+from harness import oracle_mirror, owners_mirror, read_blocks, rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -49,10 +49,10 @@ def _local_attention_reader(st):
                                                           (1, 1.0, "overlap", 1),
                                                           (1, 0.8, "serial", 2)])
 def test_bursty_trace_scaled_matches_oracle(ema, layout, local_frac, mode, group):
-    from bursty import BurstyTrace
+    from workloads.bursty import BurstyTrace
     print(f"bursty scaled layout={layout} local_frac={local_frac} mode={mode} group={group}",
           flush=True)
-    tr = BurstyTrace(synth.BURSTY, layers=4, batch=8, fill="host", mirror="data",
+    tr = BurstyTrace(synth.BURSTY, layers=4, batch=8, fill="host", mirror=oracle_mirror,
                      slice_layout=layout, local_frac=local_frac, mode=mode, group=group)
     try:
         st = tr.mirror
@@ -98,9 +98,9 @@ def test_bursty_trace_scaled_matches_oracle(ema, layout, local_frac, mode, group
 
 
 def test_bursty_trace_full_size(ema):
-    from bursty import BurstyTrace
+    from workloads.bursty import BurstyTrace
     print("bursty full size", flush=True)
-    tr = BurstyTrace(synth.BURSTY, fill="device", mirror="owners")
+    tr = BurstyTrace(synth.BURSTY, fill="device", mirror=owners_mirror)
     try:
         fp0 = tr.fingerprints()
         ms = []

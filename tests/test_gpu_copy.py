@@ -25,7 +25,7 @@ def ema():
 
 
 def i32(a):
-    return torch.as_tensor(np.asarray(a, dtype=np.int32), device="cuda")
+    return torch.as_tensor(np.ascontiguousarray(a, dtype=np.int32), device="cuda")
 
 
 class GpuBackend:

@@ -13,7 +13,7 @@ import torch
 
 import oracle
 import synth
-from harness import TORCH_DT, Workload, rel_err
+from harness import TORCH_DT, Workload, oracle_mirror, rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -29,7 +29,7 @@ def ema():
 
 
 def i32(a):
-    return torch.as_tensor(np.asarray(a, dtype=np.int32), device="cuda")
+    return torch.as_tensor(np.ascontiguousarray(a, dtype=np.int32), device="cuda")
 
 
 def u16_dev(a, dtype):
@@ -154,7 +154,7 @@ def test_decode_steps_with_append_and_writeback_match_oracle(ema, layout):
     w = Workload(cfg, layers=L, lens=lens0, slice_layout=layout, fill="host",
                  stage_n=grow + 64, extra_local=L * grow, extra_slice=L * grow)
     try:
-        st = w.oracle_mirror()
+        st = oracle_mirror(w)
         rng = np.random.default_rng(11 + layout)
         bs, nl = w.bs, w.n_local
         width = w.maxblk + steps // bs + 2

@@ -27,9 +27,10 @@ def ema():
 @pytest.mark.parametrize("bs,layout,n_blocks", [(16, 0, None), (64, 0, None), (256, 0, None),
                                                 (16, 1, 65536), (64, 1, 16384), (256, 1, 4096)])
 def test_stress_prefetch_and_reclaim_sweep(ema, bs, layout, n_blocks):
-    from stress import StressRun
+    from harness import owners_mirror
+    from workloads.stress import StressRun
     print(f"stress bs={bs} layout={layout} n_blocks={n_blocks}", flush=True)
-    run = StressRun(bs, n_blocks=n_blocks, slice_layout=layout, mirror=True)
+    run = StressRun(bs, n_blocks=n_blocks, slice_layout=layout, mirror=owners_mirror)
     try:
         pf = run.prefetch_all(reps=1)
         assert pf["exact"], "prefetch: sampled blocks differ"

@@ -10,7 +10,7 @@ import torch
 
 import oracle
 import synth
-from harness import Workload, rel_err
+from harness import Workload, oracle_mirror, rel_err
 
 pytestmark = pytest.mark.gpu
 TOL = 2e-3
@@ -40,7 +40,7 @@ def test_noalloc_equals_the_ordinary_call_on_two_calls_in_a_row(ema, hq, hkv, bs
                          700 + bs)
     w = Workload(cfg, lens=lens.tolist(), staging_slots=1)
     try:
-        st = w.oracle_mirror()
+        st = oracle_mirror(w)
         w.prefetch(0)
         st.prefetch(w.pf_src[0], w.pf_dst[0])
         small = max(1, batch // 4)

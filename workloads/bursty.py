@@ -21,8 +21,9 @@ little room for write-back and preempts sequences.
 
 After each step the caller can check the library's owners and tables: the
 device-rewritten tables against the host's own application of the returned
-moves and victims, the ownership invariants, and (with a mirror) an oracle
-replaying every operation.
+moves and victims, the ownership invariants, and (with ``mirror``, a callable
+that makes an observer of the workload -- the tests pass an oracle) a replay of
+every operation compared after each.
 """
 import math
 
@@ -30,7 +31,9 @@ import numpy as np
 import torch
 
 import synth
-from harness import StepRunner, Workload, TORCH_DT
+from paper_2609_27040_amd.kvcache import TORCH_DT
+from paper_2609_27040_amd.step import StepRunner
+from workloads.synthetic import Workload
 from paper_2609_27040_amd import ema
 
 
@@ -73,17 +76,8 @@ class BurstyTrace:
         self.readmitted = set()
         self.waiting = set()
         self.len0 = w.lens.copy()
-        self.mirror = None
-        if mirror == "data":
-            self.mirror = w.oracle_mirror()
-        elif mirror == "owners":
-            import oracle
-            st = oracle.SliceOracle(w.hkv, w.D, w.bs, cfg.dtype, w.slice_layout,
-                                    w.local_view.shape[0] * w.bb, w.slice_view.shape[0] * w.bb,
-                                    with_data=False)
-            for pool, owners in w.alloc_log:
-                st.alloc_blocks(pool, owners)
-            self.mirror = st
+        # an observer (the tests pass an oracle) replaying every operation
+        self.mirror = mirror(w) if mirror is not None else None
         if self.mirror is not None:
             self.mtables = w.tables.copy()
 

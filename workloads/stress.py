@@ -21,7 +21,8 @@ import numpy as np
 import torch
 
 import synth
-from harness import BlockedTimer, Workload
+from paper_2609_27040_amd.step import BlockedTimer
+from workloads.synthetic import Workload
 from paper_2609_27040_amd import ema
 
 FRACTIONS = (0.01, 0.05, 0.25, 1.0)
@@ -34,7 +35,7 @@ def stress_blocks(cfg, bs):
 
 class StressRun:
     def __init__(self, bs, n_blocks=None, seqs=1024, slice_layout=ema.LAYOUT_ATTN,
-                 cfg=synth.STRESS, samples=256, mirror=False):
+                 cfg=synth.STRESS, samples=256, mirror=None):
         N = stress_blocks(cfg, bs) if n_blocks is None else int(n_blocks)
         per_seq = max(1, N // seqs)
         tok = per_seq * bs
@@ -48,17 +49,10 @@ class StressRun:
         self.s = torch.cuda.Stream()
         self.timer = BlockedTimer()
         self.ns_per_mover = 50.0        # host planning estimate, refined as reclaims run
-        # an oracle without block data replaying every allocation, free, lend,
-        # migration and reclaim: plans and tables are compared with it
-        self.mirror = None
-        if mirror:
-            import oracle
-            st = oracle.SliceOracle(w.hkv, w.D, w.bs, c.dtype, slice_layout,
-                                    w.local_view.shape[0] * w.bb, w.slice_view.shape[0] * w.bb,
-                                    with_data=False)
-            for pool, owners in w.alloc_log:
-                st.alloc_blocks(pool, owners)
-            self.mirror = st
+        # an observer (the tests pass an oracle without block data) replaying
+        # every allocation, free, lend, migration and reclaim
+        self.mirror = mirror(w) if mirror is not None else None
+        if self.mirror is not None:
             self.mtables = w.tables.copy()
 
     # ---- helpers ---------------------------------------------------------------------
@@ -189,7 +183,8 @@ class StressRun:
 RUN_BLOCKS = (1, 4, 16, 64, 100, 200, 400)
 
 
-def run_sweep(bs=16, n_blocks=1 << 17, run_blocks=RUN_BLOCKS, reps=3):
+def run_sweep(bs=16, n_blocks=1 << 17, run_blocks=RUN_BLOCKS, reps=3,
+              engines=("kernel", "dma")):
     """Prefetch of every slice block as contiguous runs of R blocks (the slab x
     layer-group chunks of a layer-group-major slice), by the gather kernel and
     by the copy engines. Slice slots are taken in order (every slot is owned:
@@ -211,6 +206,8 @@ def run_sweep(bs=16, n_blocks=1 << 17, run_blocks=RUN_BLOCKS, reps=3):
             nbytes = 2 * k * R * w.bb
             rec = {"run_blocks": R, "run_bytes": R * w.bb, "runs": int(k)}
             for name, eng in (("kernel", ema.ENGINE_KERNEL), ("dma", ema.ENGINE_DMA)):
+                if name not in engines:
+                    continue
                 call = lambda: ema.slice_prefetch_runs(w.h, src_first, dst_first, runs, eng,
                                                        stream=run.s)
                 dev, wall = [], []
