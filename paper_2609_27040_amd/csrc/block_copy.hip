@@ -65,10 +65,24 @@ __device__ __forceinline__ void wave_lds_sync() {
   __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 }
 
+// Source and destination of copy i (wave-uniform i).
+__device__ __forceinline__ void copy_ids(const CopyIds& c, int32_t i, int32_t& s, int32_t& d) {
+  if (c.n_runs > 0) {
+    int r = 0;
+    for (int q = 1; q < c.n_runs; ++q)
+      if (c.run_off[q] <= i) r = q;
+    s = c.run_src[r] + (i - c.run_off[r]);
+    d = c.run_dst[r] + (i - c.run_off[r]);
+  } else {
+    s = c.src[i];
+    d = c.dst ? c.dst[i] : c.dst_base + i;
+  }
+}
+
 // The table-rewrite share of a reclaim launch: workgroup g rewrites entries
 // [g * kRewriteEntries, (g + 1) * kRewriteEntries), threads strided so that
 // reads and writes stay coalesced. Only changed entries are written.
-__device__ __forceinline__ void rewrite_tables(const TableRewrite& rw, int g) {
+__device__ __forceinline__ void rewrite_tables(const TableRewrite& rw, const CopyIds& ids, int g) {
   const int64_t e0 = int64_t(g) * kRewriteEntries;
   const int64_t e1 = e0 + kRewriteEntries < rw.n_entries ? e0 + kRewriteEntries : rw.n_entries;
   for (int64_t e = e0 + threadIdx.x; e < e1; e += blockDim.x) {
@@ -77,7 +91,15 @@ __device__ __forceinline__ void rewrite_tables(const TableRewrite& rw, int g) {
     int32_t nt = t;
     const uint32_t r = uint32_t(t - rw.base);
     if (r < uint32_t(rw.n_range)) {
-      nt = rw.range_map[r];
+      if (rw.range_map) {
+        nt = rw.range_map[r];
+      } else {                                   // movers: the launch's copy runs
+        for (int q = 0; q < ids.n_runs; ++q) {
+          const int32_t o = t - ids.run_src[q];
+          const int32_t len = ids.run_off[q + 1] - ids.run_off[q];
+          if (o >= 0 && o < len) nt = ids.run_dst[q] + o;
+        }
+      }
     } else if (rw.n_victims > 0) {
       int lo = 0, hi = rw.n_victims;               // first victim >= t
       while (lo < hi) {
@@ -91,14 +113,12 @@ __device__ __forceinline__ void rewrite_tables(const TableRewrite& rw, int g) {
   }
 }
 
-__global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
-                                                         const int32_t* __restrict__ src_ids,
-                                                         const int32_t* __restrict__ dst_ids,
+__global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv, CopyIds ids,
                                                          int32_t n, int32_t* err_count,
-                                                         TableRewrite rw, int32_t dst_base) {
+                                                         TableRewrite rw) {
   extern __shared__ __attribute__((aligned(16))) uint16_t lds_tile[];
   if (int(blockIdx.x) < rw.n_groups) {
-    rewrite_tables(rw, blockIdx.x);
+    rewrite_tables(rw, ids, blockIdx.x);
     return;
   }
   const int lane = threadIdx.x & 63;
@@ -108,8 +128,8 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
   if (unit >= int64_t(n) * upb) return;
   const int32_t i = int32_t(unit / upb);
   const int k = int(unit - int64_t(i) * upb);
-  const int32_t s = src_ids[i];
-  const int32_t d = dst_ids ? dst_ids[i] : dst_base + i;
+  int32_t s, d;
+  copy_ids(ids, __builtin_amdgcn_readfirstlane(i), s, d);
   const int32_t n_total = pv.n_local + pv.n_slice;
   if (s < 0 || s >= n_total || d < 0 || d >= n_total) {
     if (k == 0 && lane == 0) atomicAdd(err_count, 1);
@@ -258,14 +278,11 @@ __global__ __launch_bounds__(256) void block_copy_kernel(PoolView pv,
 // (blockDim.x / 64 waves each) moves piece g * (blockDim.x / 64) + w, 2 KiB of
 // block src_ids[i] to the same offset of block dst_ids[i]. Out-of-range ids
 // are skipped and counted once per block.
-__global__ __launch_bounds__(256) void block_copy_same_kernel(PoolView pv,
-                                                              const int32_t* __restrict__ src_ids,
-                                                              const int32_t* __restrict__ dst_ids,
+__global__ __launch_bounds__(256) void block_copy_same_kernel(PoolView pv, CopyIds ids,
                                                               int32_t n, int32_t* err_count,
-                                                              TableRewrite rw,
-                                                              int32_t dst_base) {
+                                                              TableRewrite rw) {
   if (int(blockIdx.x) < rw.n_groups) {
-    rewrite_tables(rw, blockIdx.x);
+    rewrite_tables(rw, ids, blockIdx.x);
     return;
   }
   const int lane = threadIdx.x & 63;
@@ -275,8 +292,8 @@ __global__ __launch_bounds__(256) void block_copy_same_kernel(PoolView pv,
   if (piece >= int64_t(n) * ppb) return;
   const int32_t i = int32_t(piece / ppb);
   const int k = int(piece - int64_t(i) * ppb);
-  const int32_t s = src_ids[i];
-  const int32_t d = dst_ids ? dst_ids[i] : dst_base + i;
+  int32_t s, d;
+  copy_ids(ids, __builtin_amdgcn_readfirstlane(i), s, d);
   const int32_t n_total = pv.n_local + pv.n_slice;
   if (s < 0 || s >= n_total || d < 0 || d >= n_total) {
     if (k == 0 && lane == 0) atomicAdd(err_count, 1);
@@ -324,9 +341,10 @@ __global__ __launch_bounds__(128) void kv_append_kernel(PoolView pv, const uint1
 
 }  // namespace
 
-hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32_t* dst,
-                             int32_t n, int32_t* err_count, hipStream_t stream, bool runs,
-                             const TableRewrite* rw, int32_t dst_base) {
+namespace {
+
+hipError_t launch_copy(const PoolView& pv, CopyIds ids, int32_t n, int32_t* err_count,
+                       hipStream_t stream, bool runs, const TableRewrite* rw) {
   TableRewrite rwl;
   if (rw && rw->n_entries > 0) {
     rwl = *rw;
@@ -340,28 +358,63 @@ hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32
                                                                                         : kWaves;
   const size_t lds = same ? 0 : size_t(kWaves) * tile_elems(pv.block_size) * 2;
   // A launch stays below 2^32 work-items: at most 2^25 wavefronts. The table
-  // rewrite rides on the first launch.
+  // rewrite rides on the first launch; lists are split, run plans always fit.
   const int64_t max_blocks = std::max<int64_t>(1, (int64_t(1) << 25) / upb);
+  if (ids.n_runs > 0 && n > max_blocks) return hipErrorInvalidValue;
   int64_t b0 = 0;
   do {
     const int32_t m = int32_t(std::max<int64_t>(0, std::min<int64_t>(max_blocks, n - b0)));
     const int64_t grid = (int64_t(m) * upb + wg_waves - 1) / wg_waves + rwl.n_groups;
     const unsigned threads = same ? unsigned(64 * wg_waves) : 256u;
-    const int32_t* s0 = m ? src + b0 : nullptr;
-    const int32_t* d0 = m && dst ? dst + b0 : nullptr;
-    const int32_t base0 = dst ? 0 : int32_t(dst_base + b0);
+    CopyIds part = ids;
+    if (ids.n_runs == 0) {
+      part.src = m ? ids.src + b0 : nullptr;
+      part.dst = m && ids.dst ? ids.dst + b0 : nullptr;
+      part.dst_base = ids.dst ? 0 : int32_t(ids.dst_base + b0);
+    }
     if (same)
       hipLaunchKernelGGL(block_copy_same_kernel, dim3(unsigned(grid)), dim3(threads), 0, stream,
-                         pv, s0, d0, m, err_count, rwl, base0);
+                         pv, part, m, err_count, rwl);
     else
       hipLaunchKernelGGL(block_copy_kernel, dim3(unsigned(grid)), dim3(threads), lds, stream, pv,
-                         s0, d0, m, err_count, rwl, base0);
+                         part, m, err_count, rwl);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     rwl.n_groups = 0;
     b0 += m;
   } while (b0 < n);
   return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32_t* dst,
+                             int32_t n, int32_t* err_count, hipStream_t stream, bool runs,
+                             const TableRewrite* rw, int32_t dst_base) {
+  CopyIds ids;
+  ids.src = src;
+  ids.dst = dst;
+  ids.dst_base = dst_base;
+  return launch_copy(pv, ids, n, err_count, stream, runs, rw);
+}
+
+hipError_t launch_block_copy_runs(const PoolView& pv, const int32_t* src_first,
+                                  const int32_t* dst_first, const int32_t* len, int32_t n_runs,
+                                  int32_t* err_count, hipStream_t stream,
+                                  const TableRewrite* rw) {
+  if (n_runs < 0 || n_runs > kArgRuns) return hipErrorInvalidValue;
+  CopyIds ids;
+  ids.n_runs = n_runs;
+  int64_t n = 0;
+  for (int32_t r = 0; r < n_runs; ++r) {
+    ids.run_src[r] = src_first[r];
+    ids.run_dst[r] = dst_first[r];
+    ids.run_off[r] = int32_t(n);
+    n += len[r];
+  }
+  ids.run_off[n_runs] = int32_t(n);
+  if (n > INT32_MAX) return hipErrorInvalidValue;
+  return launch_copy(pv, ids, int32_t(n), err_count, stream, true, rw);
 }
 
 hipError_t launch_kv_append(const PoolView& pv, const void* k_new, const void* v_new,

@@ -196,6 +196,26 @@ void release(ema_slice* h) {
   delete h;
 }
 
+// Contiguous runs of a copy list (src[i + 1] == src[i] + 1 and likewise dst),
+// or false when there are more than max_runs of them.
+bool list_runs(const std::vector<int32_t>& src, const std::vector<int32_t>& dst, int max_runs,
+               std::vector<int32_t>* rs, std::vector<int32_t>* rd, std::vector<int32_t>* rn) {
+  rs->clear();
+  rd->clear();
+  rn->clear();
+  for (size_t i = 0; i < src.size(); ++i) {
+    if (!rn->empty() && rs->back() + rn->back() == src[i] && rd->back() + rn->back() == dst[i]) {
+      ++rn->back();
+      continue;
+    }
+    if (int(rn->size()) == max_runs) return false;
+    rs->push_back(src[i]);
+    rd->push_back(dst[i]);
+    rn->push_back(1);
+  }
+  return true;
+}
+
 // The plan upload area (h_work -> d_work) is shared by reclaim and run
 // prefetches, which may be issued on different streams. begin_upload waits on
 // the host until the previous upload has left h_work, and makes `st` wait on
@@ -460,6 +480,12 @@ int ema_slice_prefetch_runs(ema_slice_t h, const int32_t* src_first, const int32
     }
     return EMA_OK;
   }
+  if (n_runs <= ema::kArgRuns) {      // the runs travel in the launch arguments
+    HIP_TRY(ema::launch_block_copy_runs(pool_view(h), src_first, dst_first, run_blocks, n_runs,
+                                        h->d_err, st),
+            "prefetch_runs launch");
+    return EMA_OK;
+  }
   if (size_t(2) * n > h->h_work_cap || size_t(2) * n > h->work_cap)
     return fail(EMA_ERR_INVAL, "prefetch_runs: more blocks than the plan buffer holds");
   if ((rc = begin_upload(h, st))) return rc;
@@ -556,10 +582,27 @@ int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, in
   const bool rewrite = n_entries > 0 && (m > 0 || nv > 0);
   if (m == 0 && !rewrite) return EMA_OK;
 
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  // Few runs and no preemption (the usual reclaim of a contiguous range): the
+  // runs travel in the launch arguments and the rewrite maps the range through
+  // them, with no upload at all.
+  std::vector<int32_t> rs, rd, rn;
+  if (nv == 0 && list_runs(plan.move_src, plan.move_dst, ema::kArgRuns, &rs, &rd, &rn)) {
+    ema::TableRewrite rw;
+    if (rewrite) {
+      rw.tables = canon_tables;
+      rw.n_entries = n_entries;
+      rw.base = h->book.n_local() + plan.cut;
+      rw.n_range = plan.reclaimed;
+    }
+    HIP_TRY(ema::launch_block_copy_runs(pool_view(h), rs.data(), rd.data(), rn.data(),
+                                        int32_t(rn.size()), h->d_err, st, &rw),
+            "reclaim launch");
+    return EMA_OK;
+  }
   // Upload: move sources [m] | destinations [m] | remap of the returned range
   // [n'] | released blocks outside the range, ascending [nvo]. One launch then
   // copies the movers and (its first workgroups) rewrites the tables.
-  hipStream_t st = static_cast<hipStream_t>(stream);
   const int32_t n_range = plan.reclaimed;
   const int32_t base = h->book.n_local() + plan.cut;
   std::vector<int32_t> vout;
@@ -930,6 +973,16 @@ int ema_slab_prefetch_group(ema_slice_t h, int32_t group, int32_t staging_first,
               "slab_prefetch_group copy");
     }
     return EMA_OK;
+  }
+  {
+    std::vector<int32_t> rs, rd, rn;
+    slab_runs(h, group, staging_first, &rs, &rd, &rn);
+    if (int(rn.size()) <= ema::kArgRuns) {   // few runs: in the launch arguments
+      HIP_TRY(ema::launch_block_copy_runs(pool_view(h), rs.data(), rd.data(), rn.data(),
+                                          int32_t(rn.size()), h->d_err, st),
+              "slab_prefetch_group launch");
+      return EMA_OK;
+    }
   }
   if (h->slab_built != h->book.slab_version()) {
     // every group's sources, rebuilt only when the set of borrowed slabs changed

@@ -31,11 +31,26 @@ struct TableRewrite {
   const int32_t* range_map = nullptr;
   const int32_t* victims = nullptr;
   int32_t base = 0;
-  int32_t n_range = 0;
+  int32_t n_range = 0;            // range_map == nullptr: the range maps through the
+                                  // launch's copy runs (t in run r -> run_dst[r] + offset)
   int32_t n_victims = 0;
   int32_t n_groups = 0;
 };
 constexpr int kRewriteEntries = 8192;   // table entries per rewriting workgroup
+
+// Where copy i's source and destination come from: device id lists, or a few
+// contiguous runs carried in the launch's own arguments, so that a plan of
+// long runs (a reclaim of a contiguous range, a slab swap) needs no upload.
+constexpr int kArgRuns = 24;
+struct CopyIds {
+  const int32_t* src = nullptr;   // device [n] (n_runs == 0)
+  const int32_t* dst = nullptr;   // device [n]; nullptr: dst_base + i (n_runs == 0)
+  int32_t dst_base = 0;
+  int32_t n_runs = 0;             // > 0: copy i lies in run r, run_off[r] <= i < run_off[r + 1]
+  int32_t run_src[kArgRuns] = {};
+  int32_t run_dst[kArgRuns] = {};
+  int32_t run_off[kArgRuns + 1] = {};
+};
 
 // dst[i] <- src[i] for i < n (unified ids), re-laid between pool layouts.
 // Ids outside [0, n_local + n_slice) are skipped and counted in *err_count.
@@ -48,6 +63,12 @@ hipError_t launch_block_copy(const PoolView& pv, const int32_t* src, const int32
                              int32_t n, int32_t* err_count, hipStream_t stream,
                              bool runs = false, const TableRewrite* rw = nullptr,
                              int32_t dst_base = 0);
+// The same for n copies given as contiguous runs (src_first[r], dst_first[r],
+// len[r]), r < n_runs <= kArgRuns, carried in the launch arguments.
+hipError_t launch_block_copy_runs(const PoolView& pv, const int32_t* src_first,
+                                  const int32_t* dst_first, const int32_t* len, int32_t n_runs,
+                                  int32_t* err_count, hipStream_t stream,
+                                  const TableRewrite* rw = nullptr);
 
 // New decode token of every sequence into its block (ATTN layout): row
 // (len-1) % bs of local block table[b][(len-1) / bs], len = seq_lens[b] > 0.
