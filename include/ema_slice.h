@@ -269,10 +269,12 @@ int ema_kv_append(ema_slice_t h, const void* k_new, const void* v_new, const int
  * preempted owners in order; moves_src/moves_dst (host [moves_cap], may be
  * NULL): the copies made. Counts beyond a cap are still reported in result.
  * In host-only mode canon_tables must be NULL with n_entries 0.
- * Device work: one upload of the plan (4 bytes per mover twice, per slot of
- * the returned range, per released block outside it) from the handle's
- * pinned buffer, then one launch that copies the movers and, in its first
- * workgroups, rewrites the tables. The upload area is shared with run
+ * Device work: when nothing is preempted and the movers form at most 24
+ * contiguous runs, one launch with the runs in its arguments (no upload);
+ * otherwise one upload of the plan (4 bytes per mover twice, per slot of the
+ * returned range, and a bitmap over the span of the released blocks outside
+ * it) from the handle's pinned buffer, then one launch that copies the movers
+ * and, in its first workgroups, rewrites the tables. The upload area is shared with run
  * prefetches (see the conventions above): before overwriting it, a reclaim
  * waits on the host for the previous upload to leave the pinned buffer and
  * makes `stream` wait for the kernels that read the previous plan.
@@ -466,7 +468,8 @@ int ema_slab_prefetch_group(ema_slice_t h, int32_t group, int32_t staging_first,
  * naming a released block becomes -1; no data moves. slabs[slabs_cap] and
  * victims[victims_cap] (host, may be NULL) get the slabs taken and the
  * preempted sequences in order. In host-only mode canon_tables must be NULL.
- * The rewrite list uses the handle's plan upload area (see the conventions).
+ * The released blocks travel as a bitmap over their span, through the
+ * handle's plan upload area (see the conventions).
  * Errors: INVAL, HIP (after the bookkeeping took effect, as for reclaim).
  */
 int ema_slab_reclaim(ema_slice_t h, int32_t n_slabs, int32_t* canon_tables, int64_t n_entries,

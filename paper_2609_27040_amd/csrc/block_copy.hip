@@ -100,14 +100,9 @@ __device__ __forceinline__ void rewrite_tables(const TableRewrite& rw, const Cop
           if (o >= 0 && o < len) nt = ids.run_dst[q] + o;
         }
       }
-    } else if (rw.n_victims > 0) {
-      int lo = 0, hi = rw.n_victims;               // first victim >= t
-      while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        if (rw.victims[mid] < t) lo = mid + 1;
-        else hi = mid;
-      }
-      if (lo < rw.n_victims && rw.victims[lo] == t) nt = -1;
+    } else if (uint32_t(t - rw.bits_base) < uint32_t(rw.n_bits)) {
+      const uint32_t b = uint32_t(t - rw.bits_base);
+      if ((rw.released_bits[b >> 5] >> (b & 31)) & 1u) nt = -1;
     }
     if (nt != t) rw.tables[e] = nt;
   }

@@ -216,6 +216,30 @@ bool list_runs(const std::vector<int32_t>& src, const std::vector<int32_t>& dst,
   return true;
 }
 
+// A set of block ids as a bitmap over [base, base + n): bit i of word i / 32
+// stands for id base + i.
+struct Bits {
+  int32_t base = 0;
+  int32_t n = 0;
+  size_t words = 0;
+};
+Bits bit_span(const std::vector<int32_t>& ids) {
+  Bits b;
+  if (ids.empty()) return b;
+  const auto mm = std::minmax_element(ids.begin(), ids.end());
+  b.base = *mm.first;
+  b.n = *mm.second - *mm.first + 1;
+  b.words = (size_t(b.n) + 31) / 32;
+  return b;
+}
+void put_bits(const std::vector<int32_t>& ids, const Bits& b, uint32_t* w) {
+  std::fill(w, w + b.words, 0u);
+  for (int32_t u : ids) {
+    const uint32_t i = uint32_t(u - b.base);
+    w[i >> 5] |= 1u << (i & 31);
+  }
+}
+
 // The plan upload area (h_work -> d_work) is shared by reclaim and run
 // prefetches, which may be issued on different streams. begin_upload waits on
 // the host until the previous upload has left h_work, and makes `st` wait on
@@ -601,16 +625,15 @@ int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, in
     return EMA_OK;
   }
   // Upload: move sources [m] | destinations [m] | remap of the returned range
-  // [n'] | released blocks outside the range, ascending [nvo]. One launch then
+  // [n'] | bitmap of the released blocks outside the range. One launch then
   // copies the movers and (its first workgroups) rewrites the tables.
   const int32_t n_range = plan.reclaimed;
   const int32_t base = h->book.n_local() + plan.cut;
   std::vector<int32_t> vout;
   for (int32_t u : plan.victim_blocks)
     if (u < base || u >= base + n_range) vout.push_back(u);
-  std::sort(vout.begin(), vout.end());
-  const int32_t nvo = int32_t(vout.size());
-  const size_t need = size_t(2) * m + (rewrite ? size_t(n_range) + nvo : 0);
+  const Bits bits = bit_span(vout);
+  const size_t need = size_t(2) * m + (rewrite ? size_t(n_range) + bits.words : 0);
   // movers, the range and released blocks are within n_total, so the buffers
   // sized at create always hold the plan
   if (need > h->h_work_cap || need > h->work_cap)
@@ -625,7 +648,7 @@ int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, in
     for (int32_t i = 0; i < m; ++i) rmap[plan.move_src[i] - base] = plan.move_dst[i];
     for (int32_t u : plan.victim_blocks)
       if (u >= base && u < base + n_range) rmap[u - base] = -1;
-    std::copy(vout.begin(), vout.end(), rmap + n_range);
+    put_bits(vout, bits, reinterpret_cast<uint32_t*>(rmap + n_range));
   }
   if ((rc = upload(h, need, st))) return rc;
   ema::TableRewrite rw;
@@ -633,10 +656,11 @@ int ema_slice_reclaim(ema_slice_t h, int32_t n_blocks, int32_t* canon_tables, in
     rw.tables = canon_tables;
     rw.n_entries = n_entries;
     rw.range_map = h->d_work + 2 * size_t(m);
-    rw.victims = h->d_work + 2 * size_t(m) + n_range;
+    rw.released_bits = reinterpret_cast<const uint32_t*>(h->d_work + 2 * size_t(m) + n_range);
     rw.base = base;
     rw.n_range = n_range;
-    rw.n_victims = nvo;
+    rw.bits_base = bits.base;
+    rw.n_bits = bits.n;
   }
   HIP_TRY(ema::launch_block_copy(pool_view(h), h->d_work, h->d_work + m, m, h->d_err, st, true,
                                  &rw),
@@ -1042,17 +1066,19 @@ int ema_slab_reclaim(ema_slice_t h, int32_t n_slabs, int32_t* canon_tables, int6
   // every released block's table entries become -1 (no data moves: the
   // preempted requests are dropped)
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const size_t need = plan.released.size();
+  const Bits bits = bit_span(plan.released);
+  const size_t need = bits.words;
   if (need > h->h_work_cap || need > h->work_cap)
     return fail(EMA_ERR_INVAL, "slab_reclaim: plan larger than the work buffers");
   if ((rc = begin_upload(h, st))) return rc;
-  std::copy(plan.released.begin(), plan.released.end(), h->h_work);
+  put_bits(plan.released, bits, reinterpret_cast<uint32_t*>(h->h_work));
   if ((rc = upload(h, need, st))) return rc;
   ema::TableRewrite rw;
   rw.tables = canon_tables;
   rw.n_entries = n_entries;
-  rw.victims = h->d_work;
-  rw.n_victims = int32_t(need);
+  rw.released_bits = reinterpret_cast<const uint32_t*>(h->d_work);
+  rw.bits_base = bits.base;
+  rw.n_bits = bits.n;
   HIP_TRY(ema::launch_block_copy(pool_view(h), nullptr, nullptr, 0, h->d_err, st, true, &rw),
           "slab_reclaim rewrite");
   return end_upload(h, st);

@@ -23,17 +23,20 @@ struct PoolView {
 // reclaim's copy launch (so the rewrite costs no launch of its own): every
 // entry t of tables[n_entries] with base <= t < base + n_range becomes
 // range_map[t - base] (the mover's destination, -1 for a preempted sequence's
-// block, else t); any other t >= 0 that is in victims[n_victims] (ascending)
-// becomes -1. n_groups == 0: no rewrite.
+// block, else t); any other t >= 0 with bits_base <= t < bits_base + n_bits
+// becomes -1 when bit t - bits_base of released_bits is set (a released block
+// outside the range: one load per entry, whatever the number released).
+// n_groups == 0: no rewrite.
 struct TableRewrite {
   int32_t* tables = nullptr;
   int64_t n_entries = 0;
   const int32_t* range_map = nullptr;
-  const int32_t* victims = nullptr;
+  const uint32_t* released_bits = nullptr;
   int32_t base = 0;
   int32_t n_range = 0;            // range_map == nullptr: the range maps through the
                                   // launch's copy runs (t in run r -> run_dst[r] + offset)
-  int32_t n_victims = 0;
+  int32_t bits_base = 0;
+  int32_t n_bits = 0;
   int32_t n_groups = 0;
 };
 constexpr int kRewriteEntries = 8192;   // table entries per rewriting workgroup
