@@ -355,30 +355,58 @@ def graph_steps(w, out, runner, args):
             "replay_matches_eager": same}
 
 
-def hbm_context(torch, gib=2, reps=5):
-    """A plain torch device-to-device copy (read + write counted) and a plain
-    read (a float32 sum of 2 GiB of bf16) on this GPU in the same run, as
-    context for the fractions of 8 TB/s."""
+def calib_lib():
+    """The calibration kernels (libema_calib.so, built with the library)."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2609_27040_amd", "lib", "libema_calib.so")
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build with __graft_entry__.build()")
+    lib = ctypes.CDLL(path)
+    for f in (lib.ema_calib_read, lib.ema_calib_copy):
+        f.restype = ctypes.c_int
+    lib.ema_calib_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                   ctypes.c_void_p]
+    lib.ema_calib_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                   ctypes.c_void_p]
+    return lib
+
+
+def hbm_context(torch, gib=4, reps=5):
+    """What plain streaming gives on this GPU in the same run, as context for
+    the fractions of 8 TB/s: the calibration kernels' contiguous read and
+    copy (16-byte non-temporal accesses, whole chunks in flight; a copy counts
+    read + write) and torch's device-to-device copy."""
     n = (gib << 30) // 2
     x = torch.randn(n, device="cuda", dtype=torch.float32).to(torch.bfloat16)
     y = torch.empty_like(x)
     res = {}
-    acc = torch.empty((), device="cuda", dtype=torch.float32)
-    for name, fn, nbytes in (("torch_copy_GBps", lambda: y.copy_(x), 4 * n),
-                             ("torch_read_GBps", lambda: torch.sum(x, 0, dtype=torch.float32,
-                                                                   out=acc), 2 * n)):
+    lib = calib_lib()
+    sink = torch.empty(2 * n // 4096, device="cuda", dtype=torch.int32)
+
+    def calib(rc):
+        if rc != 0:
+            raise RuntimeError(f"calibration launch failed ({rc})")
+    stream = lambda: torch.cuda.current_stream().cuda_stream
+    for name, fn, nbytes in (
+            ("calib_read_GBps",
+             lambda: calib(lib.ema_calib_read(x.data_ptr(), 2 * n, sink.data_ptr(), stream())),
+             2 * n),
+            ("calib_copy_GBps",
+             lambda: calib(lib.ema_calib_copy(x.data_ptr(), y.data_ptr(), 2 * n, stream())),
+             4 * n),
+            ("torch_copy_GBps", lambda: y.copy_(x), 4 * n)):
         fn()
         torch.cuda.synchronize()
-        ts = []
+        # `reps` launches back to back between one event pair: the host's
+        # submission gap before the first launch is spread over all of them
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
         for _ in range(reps):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
             fn()
-            e1.record()
-            e1.synchronize()
-            ts.append(e0.elapsed_time(e1))
-        res[name] = nbytes / (float(np.median(ts)) / 1e3) / 1e9
-    del x, y
+        e1.record()
+        e1.synchronize()
+        res[name] = reps * nbytes / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del x, y, sink
     torch.cuda.empty_cache()
     return res
 
@@ -579,6 +607,10 @@ def measure_steps(w, runner, steps, warmup, timed_layers=2):
     attn_gbps = attn_b / at_mean_s / 1e9
     pf_gbps = pf_timed_b / (pf_ms.sum() / 1e3) / 1e9 if len(pf_ms) else 0.0
     step_bytes = attn_b * w.L + float(np.sum(pf_b))
+    # Time of the step's attention and prefetch calls, each as timed on its
+    # own, over the step's wall time: near 1, the device streams HBM for the
+    # whole step and a second stream has no idle time left to fill.
+    busy_s = at_mean_s * w.L + (float(np.sum(pf_b)) / (pf_gbps * 1e9) if pf_gbps else 0.0)
     return out, {
         "ms_per_step": ms_step, "tokens_per_s": w.B / (ms_step / 1e3),
         "attention": {"bytes_per_launch": attn_b, "timed_calls": int(at_calls),
@@ -590,7 +622,8 @@ def measure_steps(w, runner, steps, warmup, timed_layers=2):
                      "mean_us": float(pf_ms.mean()) * 1e3 if len(pf_ms) else 0.0,
                      "GBps": pf_gbps, "frac": pf_gbps / HBM_PEAK_GBPS},
         "step": {"bytes": step_bytes, "GBps": step_bytes / (ms_step / 1e3) / 1e9,
-                 "frac": step_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBPS}}
+                 "frac": step_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBPS,
+                 "kernel_time_share": busy_s / (ms_step / 1e3)}}
 
 
 def roofline_obj(achieved, traffic_rec, kernel, key="bytes_per_call"):
@@ -704,7 +737,8 @@ def slab_leg(points, steps=3, warmup=1):
 def ceiling_leg():
     """What this GPU's HBM gives the library's own copy on long contiguous
     runs (the kernel engine of the run prefetch, 400-block runs of 64 KiB),
-    beside torch's plain copy and plain read, in the same process."""
+    beside the calibration kernels' plain read and plain copy and torch's
+    copy, in the same process."""
     import torch
     from workloads.stress import run_sweep
     log("leg: copy ceilings")

@@ -1,9 +1,11 @@
-"""Builds libema_slice.so (the C-ABI library) in-tree for gfx950.
+"""Builds libema_slice.so (the C-ABI library) in-tree for gfx950, and
+libema_calib.so beside it (HBM calibration kernels that only the benchmark
+loads).
 
 Every source is compiled with hipcc for gfx950 only, with the packed-fp32
 instructions switched off in device code, then linked into
-paper_2609_27040_amd/lib/libema_slice.so. Run as ``python -m
-paper_2609_27040_amd.build`` or through ``__graft_entry__.build()``.
+paper_2609_27040_amd/lib/. Run as ``python -m paper_2609_27040_amd.build`` or
+through ``__graft_entry__.build()``.
 """
 import os
 import shutil
@@ -20,6 +22,8 @@ LIB = os.path.join(LIBDIR, "libema_slice.so")
 
 SOURCES = ["slice_book.cpp", "slab_book.cpp", "ema_slice.cpp", "slice_sched.cpp", "block_copy.hip",
            "paged_attention_mfma.hip", "attn_combine.hip"]
+CALIB_LIB = os.path.join(LIBDIR, "libema_calib.so")
+CALIB_SOURCES = ["hbm_calib.hip"]
 
 ARCH = "gfx950"
 FLAGS = [
@@ -46,23 +50,29 @@ def _compile(src, obj, hipcc):
     return r.stderr
 
 
-def build(verbose=False) -> str:
-    hipcc = _hipcc()
-    objdir = os.path.join(LIBDIR, "obj")
-    os.makedirs(objdir, exist_ok=True)
-    objs = [os.path.join(objdir, os.path.splitext(s)[0] + ".o") for s in SOURCES]
-    with ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        logs = list(ex.map(lambda so: _compile(so[0], so[1], hipcc), zip(SOURCES, objs)))
-    if verbose:
-        for s, log in zip(SOURCES, logs):
-            if log.strip():
-                print(f"[{s}]\n{log}", file=sys.stderr)
-    tmp = LIB + ".tmp"
+def _link(objs, lib, hipcc):
+    tmp = lib + ".tmp"
     cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose=False) -> str:
+    hipcc = _hipcc()
+    objdir = os.path.join(LIBDIR, "obj")
+    os.makedirs(objdir, exist_ok=True)
+    srcs = SOURCES + CALIB_SOURCES
+    objs = [os.path.join(objdir, os.path.splitext(s)[0] + ".o") for s in srcs]
+    with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        logs = list(ex.map(lambda so: _compile(so[0], so[1], hipcc), zip(srcs, objs)))
+    if verbose:
+        for s, log in zip(srcs, logs):
+            if log.strip():
+                print(f"[{s}]\n{log}", file=sys.stderr)
+    _link(objs[:len(SOURCES)], LIB, hipcc)
+    _link(objs[len(SOURCES):], CALIB_LIB, hipcc)
     return LIB
 
 
