@@ -204,14 +204,14 @@ int ema_slice_prefetch_runs(ema_slice_t h, const int32_t* src_first, const int32
 
 /*
  * slice_migrate -- moves logical blocks between pools, the borrower-side step of
- * dynamic sharing (section 4: segments are assigned to a user on demand and
- * may be reassigned over time; section 4.1: allocation first tries free
- * memory, so a block placed locally can later move into a lent slot and
- * back). Block dst_ids[i] <- block src_ids[i] (device [n] unified ids; each
- * destination already allocated to the source's owner; no duplicate
- * destinations; sources and destinations disjoint), re-laid into the
- * destination pool's layout. The caller then frees the sources and updates
- * its tables. Async on `stream`.
+ * dynamic sharing (section 4: each segment of the slice serves one user at a
+ * time, is handed out when needed and can change hands later; section 4.1:
+ * allocation first tries free memory, so a block placed locally can later
+ * move into a lent slot and back). Block dst_ids[i] <- block src_ids[i]
+ * (device [n] unified ids; each destination already allocated to the
+ * source's owner; no duplicate destinations; sources and destinations
+ * disjoint), re-laid into the destination pool's layout. The caller then
+ * frees the sources and updates its tables. Async on `stream`.
  * Errors (checked mode or host-only): INVAL.
  */
 int ema_slice_migrate(ema_slice_t h, const int32_t* src_ids, const int32_t* dst_ids, int32_t n,
@@ -234,16 +234,17 @@ int ema_slice_writeback(ema_slice_t h, const int32_t* staging_ids, const int32_t
  * kv_append -- a decode step stores each sequence's new token before attention
  * reads it (section 2.3 and 4.2.2: decode appends to the KV cache every step,
  * and data swapped in through the swap buffer must later be swapped out; the
- * append lands in the staged copy that the swap-out returns): for sequence b with seq_lens[b] > 0 (lengths already counting the
- * new token), the token at position p = seq_lens[b] - 1 gets K = k_new[b] and
- * V = v_new[b] in row p % block_size of local block block_table[b][p /
- * block_size]. block_table is an attention table (device [batch][max_blocks]
- * local ids): a slice-resident block is named by its staged copy, which the
- * caller then writes back with ema_slice_writeback. k_new, v_new: device
- * [batch][num_kv_heads][head_dim] in the slice's dtype. Async on `stream`.
- * Rows whose block index is >= max_blocks or whose id is not a local block are
- * skipped and counted (ema_slice_device_errors); checked mode rejects them on
- * the host first (INVAL), and host-only mode validates host arrays.
+ * append lands in the staged copy that the swap-out returns): for sequence b
+ * with seq_lens[b] > 0 (lengths already counting the new token), the token at
+ * position p = seq_lens[b] - 1 gets K = k_new[b] and V = v_new[b] in row p %
+ * block_size of local block block_table[b][p / block_size]. block_table is an
+ * attention table (device [batch][max_blocks] local ids): a slice-resident
+ * block is named by its staged copy, which the caller then writes back with
+ * ema_slice_writeback. k_new, v_new: device [batch][num_kv_heads][head_dim] in
+ * the slice's dtype. Async on `stream`. Rows whose block index is >= max_blocks
+ * or whose id is not a local block are skipped and counted
+ * (ema_slice_device_errors); checked mode rejects them on the host first
+ * (INVAL), and host-only mode validates host arrays.
  */
 int ema_kv_append(ema_slice_t h, const void* k_new, const void* v_new, const int32_t* block_table,
                   const int32_t* seq_lens, int32_t batch, int32_t max_blocks, void* stream);

@@ -3,7 +3,7 @@ INFRASTRUCTURE ONLY.
 
 The slice is cut into slabs: a slab is ``slab_blocks`` (S) KV-block positions,
 the same positions in every one of the cache's L layers, so one slab spans
-L x S layer-blocks ("slab allocation is applied uniformly across all layers").
+L x S layer-blocks (slabs are allocated alike in every layer).
 A slab belongs to one user at a time: the lender (LENDER), nobody (FREE, lent
 but unused) or the borrower (BORROWED). Inside a borrowed slab each position
 holds one logical block of one sequence -- in every layer at once -- or is
