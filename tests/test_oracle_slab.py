@@ -328,3 +328,32 @@ def test_random_slab_traces_keep_every_invariant():
             oracle.check_ownership(st, tables)
         st.reclaim(100, tables)
         oracle.check_slab_sd_symmetry(st, tables)
+
+
+# ---- the paper's worked example (tests/golden/layer_group_example.json) --------------------
+
+def test_layer_group_major_placement_reproduces_the_papers_example():
+    import json
+    import os
+    ex = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                     "layer_group_example.json")))
+    k, L = ex["group_size"], ex["layers"]
+    S, n = 3, 4
+    st = make(200, n, L=L, S=S, k=k, layout=GROUP_MAJOR)
+    # layer groups are runs of k consecutive layers
+    for g, layers in enumerate(ex["layer_groups"]):
+        assert [l for l in range(L) if l // k == g] == layers
+    # slab 0 of the group's layers, then slab 1 of the same layers, back to back
+    adj = ex["adjacent_slabs"]
+    a, b = adj["first_slab"], adj["next_slab"]
+    first = [st.slot(a, l, p) for l in adj["layers"] for p in range(S)]
+    second = [st.slot(b, l, p) for l in adj["layers"] for p in range(S)]
+    assert first == list(range(first[0], first[0] + k * S))
+    assert second == list(range(first[-1] + 1, first[-1] + 1 + k * S))
+    # with those two slabs borrowed, the group's swap is a single transfer
+    sw = ex["combined_swap"]
+    st.slab_alloc([7] * (n * S))
+    st.slab_free([i * S + p for i in range(n) if i not in sw["borrowed_slabs"] for p in range(S)])
+    runs = st.group_runs(sw["group"], 0)
+    assert len(runs) == sw["transfers"]
+    assert runs[0][2] == len(sw["borrowed_slabs"]) * k * S
