@@ -65,7 +65,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama3-8b-kv",
                     choices=["llama3-8b-kv", "llama-70b-tp8-share", "bursty-8b", "stress",
-                             "slab-sweep"])
+                             "run-sweep", "slab-sweep"])
     ap.add_argument("--mode", default="serial", choices=["serial", "overlap"],
                     help="serial: prefetches and attention on one stream; overlap: prefetches "
                          "on a second stream, ahead of attention")
@@ -554,7 +554,7 @@ def stress_main(args):
     print(json.dumps(res))
 
 
-def slab_main(args):
+def run_sweep_main(args):
     """Copy efficiency against transfer size: prefetch of every slice block of a
     block-size-16 pool (8 GiB, 60 % slice) as contiguous runs of 1 to 400
     blocks, by the gather kernel and by the copy engines; one JSON line."""
@@ -571,7 +571,7 @@ def slab_main(args):
            "value": best, "unit": "GB/s", "n_gpus": 1, "steps": 1, "warmup": 0,
            "ms_per_step": None, "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "f16", "data": "synthetic",
-           "config": {"workload": "slab-sweep", "block_size": 16, "kv_heads": 8,
+           "config": {"workload": "run-sweep", "block_size": 16, "kv_heads": 8,
                       "blocks": 1 << 17, "slice_frac": 0.6},
            "sweep": rows}
     for r in rows:
@@ -712,17 +712,20 @@ def stress_leg(block_sizes=(16, 64, 256)):
 
 def slab_leg(points, steps=3, warmup=1):
     """The 8B-shaped step on a slab-managed slice with interleaved free slabs
-    (workloads.slabs), per (slab size, layer group, engine)."""
+    (workloads.slabs), per (slab size, layer group, engine[, placement])."""
     import torch
     import synth
     from paper_2609_27040_amd import ema
     from workloads.slabs import run_point, slab_cache
     rows = []
-    for S, k, eng in points:
-        log(f"leg: slab step S={S} group={k} engine={eng}")
-        c = slab_cache(synth.LLAMA8B, S, k, engine=eng)
+    for pt in points:
+        S, k, eng = pt[:3]
+        layout = pt[3] if len(pt) > 3 else ema.SLAB_GROUP_MAJOR
+        log(f"leg: slab step S={S} group={k} engine={eng} placement={layout}")
+        c = slab_cache(synth.LLAMA8B, S, k, layout=layout, engine=eng)
         try:
             rows.append(run_point(c, steps=steps, warmup=warmup))
+            rows[-1]["placement"] = ("layer-major", "slab-major", "layer-group-major")[layout]
             if ema.slice_device_errors(c.h):
                 raise RuntimeError("slab step: kernels skipped invalid ids")
         finally:
@@ -732,6 +735,33 @@ def slab_leg(points, steps=3, warmup=1):
         log(f"  {r['ms_per_step']:.2f} ms/step, swap {r['swap_GBps']:.0f} GB/s, "
             f"{r['runs_per_step']} runs of {r['mean_run_KiB']:.0f} KiB")
     return rows
+
+
+def slab_sweep_main(args):
+    """The slab step sweep on its own (one JSON line): slabs of 1, 10 and 100
+    blocks x groups of 1, 2 and 4 layers with the gather kernel, the copy
+    engines at groups of 4, and the three placements at 10-block slabs and
+    groups of 4 with both engines."""
+    import torch
+    from paper_2609_27040_amd import ema
+    torch.cuda.set_device(0)
+    K, D = ema.ENGINE_KERNEL, ema.ENGINE_DMA
+    pts = [(S, k, K) for S in (1, 10, 100) for k in (1, 2, 4)]
+    pts += [(S, 4, D) for S in (1, 10, 100)]
+    pts += [(10, 4, e, lay) for lay in (ema.SLAB_LAYER_MAJOR, ema.SLAB_SLAB_MAJOR)
+            for e in (K, D)]
+    rows = slab_leg(pts, steps=max(1, args.steps // 4), warmup=max(1, args.warmup))
+    best = max(rows, key=lambda r: r["tokens_per_s"])
+    res = {"metric": "prefetch/reclaim GB/s + paged decode tokens/s, % of HBM roofline, 1 GPU",
+           "value": best["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1,
+           "steps": max(1, args.steps // 4), "warmup": max(1, args.warmup),
+           "ms_per_step": best["ms_per_step"], "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": "slab-sweep", "cache": "llama3-8b-kv", "slice_frac": 0.3,
+                      "best": {k: best[k] for k in ("slab_blocks", "group", "engine",
+                                                    "placement")}},
+           "sweep": rows}
+    print(json.dumps(res))
 
 
 def ceiling_leg():
@@ -765,8 +795,11 @@ def main():
     if args.workload == "stress":
         stress_main(args)
         return
+    if args.workload == "run-sweep":
+        run_sweep_main(args)
+        return
     if args.workload == "slab-sweep":
-        slab_main(args)
+        slab_sweep_main(args)
         return
     import torch
     import synth
