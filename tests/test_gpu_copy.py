@@ -253,3 +253,58 @@ def test_prefetch_runs_validation(ema):
         assert_pools_equal(gpu, st)
     finally:
         gpu.close()
+
+
+@pytest.mark.parametrize("first", ["prefetch", "reclaim"])
+def test_plan_uploads_on_two_streams_stay_ordered(ema, first):
+    """A run prefetch and a reclaim that both upload their plans through the
+    handle's shared upload area, issued on two streams with no host
+    synchronisation between them; the first call is queued behind a long copy,
+    so its kernel has not started when the second call plans and uploads. Both
+    pools and the rewritten table must equal the oracle's, which runs the two
+    calls one after the other."""
+    print(f"two-stream uploads, first={first}", flush=True)
+    n_local, n_slice = 34000, 30000
+    gpu, st = make_pair(ema, 16, 0, "bf16", n_local, n_slice, seed=77, hkv=1)
+    try:
+        nl = st.n_local
+        owners = np.arange(n_slice) % 50
+        ids = gpu.alloc_blocks(1, owners)
+        assert np.array_equal(ids, st.alloc_blocks(1, owners))
+        # every third slot below the top 3000 freed: the reclaim compacts into
+        # scattered slots (3000 runs of one block: its plan is uploaded)
+        free = ids[:27000:3]
+        gpu.free_blocks(free)
+        st.free_blocks(free)
+        stage = gpu.alloc_blocks(0, [-2] * 8000)
+        assert np.array_equal(stage, st.alloc_blocks(0, [-2] * 8000))
+        # 4000 runs of two used slice blocks each into contiguous staging
+        # (more runs than the launch arguments carry: the list is uploaded)
+        j = np.arange(4000)
+        src_first, dst_first, runs = nl + 1 + 3 * j, stage[0] + 2 * j, np.full(4000, 2)
+        table = np.setdiff1d(ids, free).astype(np.int64)
+        tdev = i32(table)
+        big = torch.empty(8 << 30, dtype=torch.uint8, device="cuda")
+        big2 = torch.empty_like(big)
+        s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s1):
+            big2.copy_(big)                            # keeps s1 busy for milliseconds
+        pf = lambda s: ema.slice_prefetch_runs(gpu.h, src_first, dst_first, runs, stream=s)
+        rc = lambda s: ema.slice_reclaim(gpu.h, 3000, tdev, stream=s)
+        if first == "prefetch":
+            pf(s1)
+            r = rc(s2)
+        else:
+            r = rc(s1)
+            pf(s2)
+        torch.cuda.synchronize()
+        del big, big2
+        for a, b in zip(src_first, dst_first):
+            st.prefetch([a, a + 1], [b, b + 1])
+        ro = st.reclaim(3000, table)
+        assert r["moved"] == ro["moved"] == 3000 and r["victims"] == ro["victims"] == []
+        assert np.array_equal(tdev.cpu().numpy(), table)
+        assert_pools_equal(gpu, st)
+    finally:
+        gpu.close()
