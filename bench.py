@@ -174,52 +174,114 @@ def attention_samples(timers, w):
     return np.array(per_call), calls
 
 
-def cpu_baseline(w, seconds):
-    """The oracle timed on this host's cores on a bounded sample: float64
-    attention of layer 0 for whole sequences, and block prefetch copies."""
-    import oracle
+def _host_blocks(w, ids):
+    """Host copies (uint8 [n][block bytes]) of unified blocks of a workload."""
     import torch
-    from threadpoolctl import threadpool_limits
+    ids = np.asarray(ids, dtype=np.int64)
+    out = np.empty((len(ids), w.bb), dtype=np.uint8)
+    loc = ids < w.n_local
+    for mask, view, off in ((loc, w.local_view, 0), (~loc, w.slice_view, w.n_local)):
+        if mask.any():
+            sel = torch.from_numpy(ids[mask] - off).to(view.device)
+            out[mask] = view[sel].cpu().numpy()
+    return out
 
-    def read_blocks(view, ids):
-        ids = np.asarray(ids, dtype=np.int64)
-        data = view[torch.from_numpy(ids).to(view.device)].cpu().numpy()
-        return {int(u): data[i] for i, u in enumerate(ids)}
 
-    rng = np.random.default_rng(0)
-    order = rng.permutation(w.B)[:16]
-    cache = {}
-    for b in order:
-        nb = (int(w.lens[b]) + w.bs - 1) // w.bs
-        cache[int(b)] = read_blocks(w.local_view, w.attn_tables[0, b, :nb])
+def _oracle_layer(w, layer, min_s):
+    """The oracle's float64 attention of every sequence of one layer over the
+    canonical table, then that layer's prefetch (one block at a time, slice
+    layout -> local layout), each repeated until it has run min_s seconds.
+    Returns (seconds per attention pass, seconds per prefetch pass, passes)."""
+    import oracle
+    tab = w.tables[layer]
+    used = np.unique(tab[tab >= 0])
+    data = _host_blocks(w, used)
+    row = {int(u): i for i, u in enumerate(used)}
+    slice_layout = w.slice_layout
+
+    def read(u):
+        blk = data[row[int(u)]]
+        if int(u) >= w.n_local and slice_layout != oracle.LAYOUT_ATTN:
+            return oracle.convert_block(blk, slice_layout, oracle.LAYOUT_ATTN, w.hkv, w.D, w.bs)
+        return blk
+    n_a, t0 = 0, time.perf_counter()
+    while n_a == 0 or time.perf_counter() - t0 < min_s:
+        oracle.paged_decode_attention(w.q16, tab, w.lens, read, w.hkv, w.D, w.bs, w.cfg.dtype)
+        n_a += 1
+    t_a = (time.perf_counter() - t0) / n_a
+    src = np.asarray(w.pf_src[layer], dtype=np.int64)
+    sdata = data[[row[int(u)] for u in src]] if len(src) else np.empty((0, w.bb), np.uint8)
+    dst = np.empty_like(sdata)
+    n_p, t0 = 0, time.perf_counter()
+    while n_p == 0 or time.perf_counter() - t0 < min_s / 4:
+        for i in range(len(sdata)):
+            dst[i] = oracle.convert_block(sdata[i], slice_layout, oracle.LAYOUT_ATTN, w.hkv,
+                                          w.D, w.bs)
+        n_p += 1
+    t_p = (time.perf_counter() - t0) / n_p
+    return t_a, t_p, len(src), n_a
+
+
+def cpu_baseline(w, seconds):
+    """The oracle timed on this host's cores (one thread) on the parts the
+    baseline plan names: the tiny config in full; one layer of the 8B-shaped
+    cache, its attention over every sequence plus that layer's prefetch; one
+    layer of the 70B TP-8 share; 4 GiB of single-block copies of the stress
+    pools' shape (64 KiB blocks). `value` is the 8B layer extrapolated to a
+    whole decode step (every layer's prefetch and attention): batch / (layers
+    x (attention + prefetch of one layer))."""
+    import torch
+    import synth
+    import oracle
+    from threadpoolctl import threadpool_info, threadpool_limits
+    from workloads.synthetic import Workload
+
+    per = max(0.5, seconds / 4)
+    res = {"unit": "tokens/s", "cores": 1, "kind": "oracle",
+           "host_cores_available": len(os.sched_getaffinity(0)),
+           "blas_threads_default": [p.get("num_threads") for p in threadpool_info()],
+           "blas_threads_used": 1}
     with threadpool_limits(1):
-        n_seq = 0
+        t_a, t_p, n_pf, reps = _oracle_layer(w, 0, per)
+        tok_s = w.B / (w.L * (t_a + t_p))
+        res["value"] = tok_s
+        res["llama3-8b-kv_layer"] = {
+            "attention_s": t_a, "prefetch_s": t_p, "prefetch_blocks": n_pf,
+            "attention_GBps": attention_bytes(w) / t_a / 1e9,
+            "prefetch_GBps": 2 * n_pf * w.bb / t_p / 1e9 if t_p > 0 else None,
+            "tokens_per_s_extrapolated": tok_s, "attention_passes": reps}
+        for cfg, key in ((synth.TINY, "tiny_full"), (synth.L70B_TP8, "llama-70b-tp8-share_layer")):
+            v = Workload(cfg, layers=1, fill="device", staging_slots=1)
+            try:
+                ta, tp, n, reps = _oracle_layer(v, 0, per if cfg is not synth.TINY else 0.5)
+                res[key] = {"attention_s": ta, "prefetch_s": tp, "prefetch_blocks": n,
+                            "attention_GBps": attention_bytes(v) / ta / 1e9,
+                            "tokens_per_s_layer": v.B / (ta + tp), "attention_passes": reps,
+                            "layers_in_config": cfg.layers}
+            finally:
+                v.close()
+                torch.cuda.empty_cache()
+        # 4 GiB of 64 KiB blocks (the stress pools at block size 16), one
+        # oracle block copy at a time
+        bb = 64 << 10
+        n_blk = (4 << 30) // bb
+        src = np.empty((n_blk, bb), dtype=np.uint8)
+        src[:] = np.arange(bb, dtype=np.uint64).astype(np.uint8)
+        dst = np.empty_like(src)
         t0 = time.perf_counter()
-        while time.perf_counter() - t0 < seconds:
-            b = int(order[n_seq % len(order)])
-            oracle.paged_decode_attention(w.q16[b:b + 1], w.attn_tables[0, b:b + 1],
-                                          w.lens[b:b + 1], cache[b].__getitem__, w.hkv, w.D,
-                                          w.bs, w.cfg.dtype)
-            n_seq += 1
-        t_attn = time.perf_counter() - t0
-        # prefetch copies (slice layout -> local layout), one block at a time
-        src = list(cache[int(order[0])].values())
-        dst = np.empty((len(src), w.bb), dtype=np.uint8)
-        n_cp = 0
-        t0 = time.perf_counter()
-        while time.perf_counter() - t0 < seconds / 4:
-            i = n_cp % len(src)
-            dst[i] = oracle.convert_block(src[i], w.slice_layout, oracle.LAYOUT_ATTN, w.hkv, w.D,
-                                          w.bs)
-            n_cp += 1
-        t_cp = time.perf_counter() - t0
-    tok_s = n_seq / t_attn / w.L      # one decode token needs every layer
-    return {"value": tok_s, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": (f"float64 attention of {n_seq} whole sequences of layer 0 "
-                       f"({t_attn:.1f} s, one thread), scaled to {w.L} layers per token; "
-                       f"{n_cp} block prefetch copies ({t_cp:.1f} s)"),
-            "prefetch_GBps": 2 * n_cp * w.bb / t_cp / 1e9,
-            "host_cores_available": len(os.sched_getaffinity(0))}
+        for i in range(n_blk):
+            dst[i] = oracle.convert_block(src[i], oracle.LAYOUT_ATTN, oracle.LAYOUT_ATTN, 8,
+                                          128, 16)
+        t_c = time.perf_counter() - t0
+        del src, dst
+        res["stress_copy_4GiB"] = {"blocks": n_blk, "seconds": t_c,
+                                   "GBps": 2 * n_blk * bb / t_c / 1e9}
+    res["sample"] = (
+        "one thread: tiny config in full; 8B-shaped layer 0 (all "
+        f"{w.B} sequences, float64 attention, {res['llama3-8b-kv_layer']['attention_passes']} "
+        f"passes) plus its prefetch of {n_pf} blocks, extrapolated to {w.L} layers; 70B-share "
+        f"layer 0 (128 sequences); 4 GiB of single-block copies ({n_blk} x 64 KiB)")
+    return res
 
 
 def cpu_copy_baseline(rows, layout, hkv, D, bs, seconds):
