@@ -91,9 +91,9 @@ def parse():
                     help="A/B pairs of the staged vs all-local attention passes (0: skip)")
     ap.add_argument("--no-legs", action="store_true",
                     help="skip the other workloads' compact legs reported beside the headline "
-                         "(70B TP-8 share step, stress prefetch, token-major slice, slab sweep, "
-                         "copy ceilings)")
-    ap.add_argument("--legs", default="c3,stress,nhd,slabs,ceiling",
+                         "(70B TP-8 share step, stress prefetch, token-major slice, bursty "
+                         "trace, slab sweep, copy ceilings)")
+    ap.add_argument("--legs", default="c3,stress,nhd,bursty,slabs,ceiling",
                     help="which compact legs to run (comma-separated)")
     return ap.parse_args()
 
@@ -496,63 +496,85 @@ def reclaim_phase(w, s, reps, ema, torch):
     return res
 
 
-def bursty_main(args):
+def bursty_run(mode="serial", group=4, steps=None):
     """The bursty elastic trace: every step the lender lends or reclaims 1-25 %
     of the slice, the borrower's slice fraction takes a random-walk step and
-    blocks migrate, then one overlapped decode step runs; prints the per-step
-    latency distribution (one JSON line)."""
+    blocks migrate, then one decode step runs; returns the per-step latency
+    distribution (the invariants are checked after every step)."""
     import torch
     import synth
     from workloads.bursty import BurstyTrace
+    from paper_2609_27040_amd import ema
 
     torch.cuda.set_device(0)
     cfg = synth.BURSTY
     log("setting up bursty-8b")
-    tr = BurstyTrace(cfg, fill="device", mode=args.mode, group=args.group)
+    tr = BurstyTrace(cfg, fill="device", mode=mode, group=group)
     w = tr.w
-    steps = cfg.extra["steps"]
+    steps = cfg.extra["steps"] if steps is None else steps
     recs, gbps = [], []
-    for k in range(steps):
-        rec = tr.step()
-        tr.check_invariants()
-        pf = sum(2 * len(s) * w.bb for s in w.pf_src)
-        toks = int(w.lens.sum())
-        attn = w.L * (toks * 2 * w.hkv * w.D * 2)
-        gbps.append((attn + pf) / (rec["ms"] / 1e3) / 1e9)
-        recs.append(rec)
-        if (k + 1) % 50 == 0:
-            log(f"step {k + 1}: {rec['ms']:.3f} ms, slice fraction {rec['slice_frac']:.2f}")
-    from paper_2609_27040_amd import ema
-    errs = ema.slice_device_errors(w.h)
-    if errs:
-        raise RuntimeError(f"kernels skipped {errs} invalid ids")
-    ms = np.array([r["ms"] for r in recs])
-    fr = np.array([r["slice_frac"] for r in recs])
-    res = {
-        "metric": "prefetch/reclaim GB/s + paged decode tokens/s, % of HBM roofline, 1 GPU",
-        "value": w.B / (float(np.median(ms)) / 1e3),
-        "unit": "tokens/s",
-        "n_gpus": 1, "steps": steps, "warmup": 0,
-        "ms_per_step": float(np.median(ms)),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": cfg.dtype, "data": "synthetic",
-        "config": {"workload": cfg.name, "layers": w.L, "batch": w.B, "q_heads": cfg.q_heads,
-                   "kv_heads": cfg.kv_heads, "head_dim": cfg.head_dim,
-                   "block_size": cfg.block_size, "lens": list(cfg.lens),
-                   "frac_max": cfg.extra["frac_max"], "step_frac": list(cfg.extra["step_frac"]),
-                   "mode": args.mode, "layer_group": args.group},
-        "step_ms": {"p10": pct(ms, 10), "p50": pct(ms, 50), "p90": pct(ms, 90),
-                    "max": float(ms.max())},
-        "step_GBps": {"p10": pct(gbps, 10), "p50": pct(gbps, 50), "p90": pct(gbps, 90)},
-        "slice_frac": {"min": float(fr.min()), "max": float(fr.max())},
-        "lender": {"reclaims": sum(1 for e in tr.log if e[0] == "reclaim"),
-                   "lends": sum(1 for e in tr.log if e[0] == "lend"),
-                   "moved_blocks": int(sum(e[2] for e in tr.log if e[0] == "reclaim")),
-                   "preempted": int(sum(len(e[4]) for e in tr.log if e[0] == "reclaim"))},
-        "migrated_blocks": int(sum(e[2] for e in tr.log if e[0] == "migrate")),
-    }
-    tr.close()
+    try:
+        for k in range(steps):
+            rec = tr.step()
+            tr.check_invariants()
+            pf = sum(2 * len(s) * w.bb for s in w.pf_src)
+            toks = int(w.lens.sum())
+            attn = w.L * (toks * 2 * w.hkv * w.D * 2)
+            gbps.append((attn + pf) / (rec["ms"] / 1e3) / 1e9)
+            recs.append(rec)
+            if (k + 1) % 50 == 0:
+                log(f"step {k + 1}: {rec['ms']:.3f} ms, slice fraction {rec['slice_frac']:.2f}")
+        errs = ema.slice_device_errors(w.h)
+        if errs:
+            raise RuntimeError(f"kernels skipped {errs} invalid ids")
+        ms = np.array([r["ms"] for r in recs])
+        fr = np.array([r["slice_frac"] for r in recs])
+        res = {
+            "value": w.B / (float(np.median(ms)) / 1e3), "unit": "tokens/s",
+            "steps": steps, "ms_per_step": float(np.median(ms)),
+            "config": {"workload": cfg.name, "layers": w.L, "batch": w.B,
+                       "q_heads": cfg.q_heads, "kv_heads": cfg.kv_heads,
+                       "head_dim": cfg.head_dim, "block_size": cfg.block_size,
+                       "lens": list(cfg.lens), "frac_max": cfg.extra["frac_max"],
+                       "step_frac": list(cfg.extra["step_frac"]), "mode": mode,
+                       "layer_group": group},
+            "step_ms": {"p10": pct(ms, 10), "p50": pct(ms, 50), "p90": pct(ms, 90),
+                        "max": float(ms.max())},
+            "step_GBps": {"p10": pct(gbps, 10), "p50": pct(gbps, 50), "p90": pct(gbps, 90)},
+            "slice_frac": {"min": float(fr.min()), "max": float(fr.max())},
+            "lender": {"reclaims": sum(1 for e in tr.log if e[0] == "reclaim"),
+                       "lends": sum(1 for e in tr.log if e[0] == "lend"),
+                       "moved_blocks": int(sum(e[2] for e in tr.log if e[0] == "reclaim")),
+                       "preempted": int(sum(len(e[4]) for e in tr.log if e[0] == "reclaim"))},
+            "migrated_blocks": int(sum(e[2] for e in tr.log if e[0] == "migrate")),
+        }
+    finally:
+        tr.close()
+        torch.cuda.empty_cache()
+    return res
+
+
+def bursty_main(args):
+    """The bursty trace on its own: one JSON line."""
+    r = bursty_run(args.mode, args.group)
+    res = {"metric": "prefetch/reclaim GB/s + paged decode tokens/s, % of HBM roofline, 1 GPU",
+           "value": r["value"], "unit": "tokens/s", "n_gpus": 1, "steps": r["steps"],
+           "warmup": 0, "ms_per_step": r["ms_per_step"], "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic"}
+    res.update({k: v for k, v in r.items() if k not in res})
     print(json.dumps(res))
+
+
+def bursty_leg(steps=100):
+    """A compact bursty trace beside the headline; its roofline is the whole
+    step's HBM rate (attention plus prefetch bytes over the step time, median
+    over steps that also reclaim, lend and migrate)."""
+    log(f"leg: bursty trace, {steps} steps")
+    r = bursty_run(steps=steps)
+    r["roofline"] = roofline_obj(r["step_GBps"]["p50"], None,
+                                 "decode step (prefetch + paged decode attention) under "
+                                 "reclaims, lends and migrations")
+    return r
 
 
 def stress_main(args):
@@ -974,8 +996,9 @@ def main():
 def run_legs(args):
     """The other workloads, compact, beside the headline (each with its own
     roofline object): the 70B TP-8 share's step, the stress pools' prefetch and
-    reclaim, the 8B step with a token-major slice (the relayout copy), the
-    slab step sweep, and the copy ceilings of this GPU."""
+    reclaim, the 8B step with a token-major slice (the relayout copy), a
+    100-step bursty trace, the slab step sweep, and the copy ceilings of this
+    GPU."""
     import synth
     want = set(args.legs.split(","))
     legs = {}
@@ -991,6 +1014,8 @@ def run_legs(args):
             synth.LLAMA8B, steps=10, warmup=2, slice_layout=1,
             counters="block_copy_token_major_prefetch_counters.md", sources=COPY_SOURCES,
             roof="prefetch")
+    if "bursty" in want:
+        legs["bursty-8b"] = bursty_leg()
     if "slabs" in want:
         from paper_2609_27040_amd import ema
         pts = [(S, k, ema.ENGINE_KERNEL) for S in (1, 10, 100) for k in (1, 2, 4)]
