@@ -345,8 +345,10 @@ int ema_paged_decode_attention_noalloc(ema_slice_t h, const void* q, const int32
                                        void* out, int32_t out_dtype, void* stream);
 
 /*
- * Synchronizes the device, then reads and clears the number of ids the
- * kernels skipped as out of range since the last call (0 when all were valid).
+ * Error accounting of the unchecked mode (no passage: a property of this
+ * library). Synchronizes the device, then reads and clears the number of ids
+ * the kernels skipped as out of range since the last call (0 when all were
+ * valid).
  */
 int ema_slice_device_errors(ema_slice_t h, int32_t* count);
 
@@ -423,6 +425,9 @@ int ema_slab_alloc(ema_slice_t h, int32_t n, const int32_t* owners, int32_t* out
 int ema_slab_free(ema_slice_t h, const int32_t* pos, int32_t n);
 
 /*
+ * Where a slab position's blocks live (sections 4.2.1-4.2.3: the placement
+ * maps a slab, layer and position to a slice slot; section 4.2.2: a swapped
+ * group is read from its copy in the swap buffer).
  * The unified ids of layer `layer`'s blocks at slab positions pos[n] (host):
  * with staging_first < 0 the slice blocks; otherwise the blocks the swap of
  * that layer's group puts them in, in the staging image that starts at local
@@ -432,6 +437,8 @@ int ema_slab_block_ids(ema_slice_t h, const int32_t* pos, int32_t n, int32_t lay
                        int32_t staging_first, int32_t* out_ids);
 
 /*
+ * The swap of a layer group as transfers (section 4.2.2: a group is swapped
+ * at once; sections 4.2.1-4.2.3 give each placement's transfer sizes).
  * The swap of layer group `group` as runs (host arrays of cap entries; any
  * may be NULL): every borrowed slab's blocks of the group's layers, used and
  * unused positions alike, into a staging image at staging_first that keeps
