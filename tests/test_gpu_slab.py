@@ -198,22 +198,24 @@ def test_swap_lists_follow_the_borrowed_set(ema):
         c.close()
 
 
+@pytest.mark.parametrize("mode", ["serial", "overlap"])
 @pytest.mark.parametrize("engine", [0, 1])
 @pytest.mark.parametrize("S,k", [(1, 1), (3, 2), (10, 4)])
-def test_slab_step_matches_the_oracle(ema, engine, S, k):
+def test_slab_step_matches_the_oracle(ema, engine, S, k, mode):
     """The bench's slab step (workloads.slabs) on a scaled-down 8B-shaped
     cache with interleaved free slabs: one full step (every group's swap and
-    every layer's attention, one stream), then every layer's attention through
+    every layer's attention, on one stream or with the swaps on a second),
+    whose last layer's output is checked, then every layer's attention through
     its staged table against the float64 oracle over the canonical blocks."""
     from paper_2609_27040_amd.step import StepRunner
     from workloads.slabs import slab_cache
-    print(f"slab step engine={engine} S={S} k={k}", flush=True)
+    print(f"slab step engine={engine} S={S} k={k} mode={mode}", flush=True)
     cfg = synth.LLAMA8B.scaled(layers=4, batch=6, lens=("uniform", 40, 300))
     c = slab_cache(cfg, S, k, engine=engine, seed=100 + S)
     try:
         runs = [c.group_runs(g) for g in range(len(c.groups))]
         assert all(int(r[2].sum()) == c.swap_blocks() for r in runs)
-        runner = StepRunner(c, "serial")
+        runner = StepRunner(c, mode)
         out = c.new_out()
         lv = c.local_view.cpu().numpy()
         sv = c.slice_view.cpu().numpy()
@@ -222,6 +224,10 @@ def test_slab_step_matches_the_oracle(ema, engine, S, k):
             return lv[u] if u < c.n_local else sv[u - c.n_local]
         runner.run(out)
         torch.cuda.synchronize()
+        last = c.L - 1
+        ref = oracle.paged_decode_attention(c.q16, c.tables[last], c.lens, read, c.hkv, D,
+                                            c.bs, c.dtype)
+        assert rel_err(out.cpu().numpy(), ref) <= 2e-3, "step output of the last layer"
         for l in range(c.L):
             # an image holds the last group swapped into it: swap l's group again
             c.prefetch_group(l // k)
