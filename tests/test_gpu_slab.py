@@ -239,3 +239,47 @@ def test_slab_step_matches_the_oracle(ema, engine, S, k, mode):
         assert ema.slice_device_errors(c.h) == 0
     finally:
         c.close()
+
+
+def test_slab_step_full_size_sampled(ema):
+    """The slab sweep's configuration at its real size (the 8B-shaped cache,
+    32 layers, batch 64, 10-block slabs, groups of 4, layer-group-major, a
+    seeded half of the slabs set aside): one full step on one stream, then for
+    three layers the attention through the staged tables on sampled sequences against the
+    float64 oracle over the canonical blocks, and the staged copies of those
+    sequences' slab blocks equal to their slice blocks."""
+    from paper_2609_27040_amd.step import StepRunner
+    from harness import read_blocks
+    from workloads.slabs import slab_cache
+    print("slab step full size", flush=True)
+    c = slab_cache(synth.LLAMA8B, 10, 4)
+    rng = np.random.default_rng(9)
+    try:
+        runner = StepRunner(c, "serial")
+        out = c.new_out()
+        runner.run(out)
+        torch.cuda.synchronize()
+        for l in (0, 17, 31):
+            c.prefetch_group(l // c.group)
+            ema.paged_decode_attention(c.h, c.q, c.attn_dev[l], c.lens_dev, out)
+            torch.cuda.synchronize()
+            got = out.cpu().numpy()
+            for b in rng.choice(c.B, size=3, replace=False):
+                nb = (int(c.lens[b]) + c.bs - 1) // c.bs
+                canon = c.tables[l, b, :nb]
+                staged = c.attn_tables[l, b, :nb]
+                loc = read_blocks(c.local_view, canon[canon < c.n_local])
+                sli = read_blocks(c.slice_view, canon[canon >= c.n_local] - c.n_local)
+
+                def read(u, loc=loc, sli=sli):
+                    return loc[int(u)] if u < c.n_local else sli[int(u) - c.n_local]
+                ref = oracle.paged_decode_attention(c.q16[b:b + 1], c.tables[l, b:b + 1],
+                                                    c.lens[b:b + 1], read, c.hkv, D, c.bs,
+                                                    c.dtype)
+                assert rel_err(got[b:b + 1], ref) <= 2e-3, (l, b)
+                st = read_blocks(c.local_view, staged[canon >= c.n_local])
+                for u, s in zip(staged[canon >= c.n_local], canon[canon >= c.n_local]):
+                    assert np.array_equal(st[int(u)], sli[int(s) - c.n_local]), (l, b, u)
+        assert ema.slice_device_errors(c.h) == 0
+    finally:
+        c.close()
