@@ -245,9 +245,9 @@ def test_slab_step_full_size_sampled(ema):
     """The slab sweep's configuration at its real size (the 8B-shaped cache,
     32 layers, batch 64, 10-block slabs, groups of 4, layer-group-major, a
     seeded half of the slabs set aside): one full step on one stream, then for
-    three layers the attention through the staged tables on sampled sequences against the
-    float64 oracle over the canonical blocks, and the staged copies of those
-    sequences' slab blocks equal to their slice blocks."""
+    three layers the attention through the staged tables on sampled sequences
+    against the float64 oracle over the canonical blocks, and the staged copies
+    of those sequences' slab blocks equal to their slice blocks."""
     from paper_2609_27040_amd.step import StepRunner
     from harness import read_blocks
     from workloads.slabs import slab_cache
