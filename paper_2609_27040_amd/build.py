@@ -41,18 +41,26 @@ def _hipcc():
     return exe
 
 
-def _compile(src, obj, hipcc):
+# Host code checked with AddressSanitizer and UBSan (device code untouched):
+# `python -m paper_2609_27040_amd.build --sanitize-host` writes
+# lib/host-sanitized/libema_slice.so, for host-only runs with clang's ASan
+# runtime preloaded.
+SAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+             "-fno-omit-frame-pointer", "-g"]
+
+
+def _compile(src, obj, hipcc, extra=()):
     lang = ["-x", "hip"] if src.endswith(".hip") else []
-    cmd = [hipcc, *FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc, *FLAGS, *extra, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
     return r.stderr
 
 
-def _link(objs, lib, hipcc):
+def _link(objs, lib, hipcc, extra=()):
     tmp = lib + ".tmp"
-    cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
+    cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *extra, *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
@@ -76,5 +84,22 @@ def build(verbose=False) -> str:
     return LIB
 
 
+def build_host_sanitized() -> str:
+    """The library with its host code built under AddressSanitizer and UBSan."""
+    hipcc = _hipcc()
+    out_dir = os.path.join(LIBDIR, "host-sanitized")
+    objdir = os.path.join(out_dir, "obj")
+    os.makedirs(objdir, exist_ok=True)
+    objs = [os.path.join(objdir, os.path.splitext(s)[0] + ".o") for s in SOURCES]
+    with ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
+        list(ex.map(lambda so: _compile(so[0], so[1], hipcc, SAN_FLAGS), zip(SOURCES, objs)))
+    lib = os.path.join(out_dir, "libema_slice.so")
+    _link(objs, lib, hipcc, SAN_FLAGS[:4])
+    return lib
+
+
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    if "--sanitize-host" in sys.argv:
+        print(build_host_sanitized())
+    else:
+        print(build(verbose="-v" in sys.argv))
