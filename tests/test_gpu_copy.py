@@ -9,7 +9,7 @@ import pytest
 import torch
 
 import oracle
-from trace import Cache, OracleBackend, random_trace
+from slice_trace import Cache, OracleBackend, random_trace
 
 pytestmark = pytest.mark.gpu
 

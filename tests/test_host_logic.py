@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 
 import oracle
-from trace import Cache, OracleBackend, random_trace
+from slice_trace import Cache, OracleBackend, random_trace
 
 LIB = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
                    "paper_2609_27040_amd", "lib", "libema_slice.so")

@@ -13,7 +13,7 @@ import pytest
 import oracle
 from oracle import FREE, STAGING, LENDER, LOCAL, SLICE
 from synth import random_16bit, pack_block, unpack_block, LAYOUT_ATTN, LAYOUT_NHD
-from trace import Cache, OracleBackend, random_trace
+from slice_trace import Cache, OracleBackend, random_trace
 
 HKV, D, BS = 2, 128, 16
 BB = 2 * BS * HKV * D * 2
