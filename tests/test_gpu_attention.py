@@ -156,6 +156,38 @@ def test_calls_with_different_cuts_on_one_handle(ema, impl):
         w.close()
 
 
+def test_empty_batch_and_all_empty_sequences(ema, impl):
+    """Degenerate calls: a batch of zero sequences launches nothing and leaves
+    the output alone; a batch whose sequences are all empty writes zeros (no
+    tile anywhere, so no range cuts a pair); a normal call on the same handle
+    afterwards still matches the oracle."""
+    print(f"degenerate batches {impl}", flush=True)
+    cfg = synth.KVConfig("degenerate", 1, 8, 2, 128, "bf16", 16, 12, ("uniform", 0, 0), 0.5, 77)
+    lens = np.random.default_rng(77).integers(1, 900, 12)
+    w = Workload(cfg, lens=lens.tolist(), staging_slots=1, attn_grid=impl == "grid")
+    try:
+        st = oracle_mirror(w)
+        w.prefetch(0)
+        st.prefetch(w.pf_src[0], w.pf_dst[0])
+        out = torch.full((12, 8, 128), float("nan"), device="cuda")
+        empty = torch.zeros(0, dtype=torch.int32, device="cuda")
+        ema.paged_decode_attention(w.h, w.q[:0], w.attn_dev[0][:0], empty, out[:0])
+        zeros = torch.zeros(12, dtype=torch.int32, device="cuda")
+        out2 = torch.full((12, 8, 128), float("nan"), device="cuda")
+        ema.paged_decode_attention(w.h, w.q, w.attn_dev[0], zeros, out2)
+        torch.cuda.synchronize()
+        assert torch.isnan(out).all()
+        assert (out2 == 0).all()
+        w.attention(0, out)
+        torch.cuda.synchronize()
+        ref = oracle.paged_decode_attention(w.q16, w.attn_tables[0], w.lens, st.read_block,
+                                            w.hkv, w.D, w.bs, w.cfg.dtype)
+        assert rel_err(out.cpu().numpy(), ref) <= TOL
+        assert ema.slice_device_errors(w.h) == 0
+    finally:
+        w.close()
+
+
 def test_wide_batch_takes_the_long_chunk_path(ema, impl):
     """batch x kv heads >= 256 selects 512-token workgroups; full oracle check."""
     print(f"wide {impl}", flush=True)
