@@ -245,12 +245,16 @@ def cpu_baseline(w, seconds):
         t_a, t_p, n_pf, reps = _oracle_layer(w, 0, per)
         tok_s = w.B / (w.L * (t_a + t_p))
         res["value"] = tok_s
-        res["llama3-8b-kv_layer"] = {
+        res[f"{w.cfg.name}_layer"] = {
             "attention_s": t_a, "prefetch_s": t_p, "prefetch_blocks": n_pf,
             "attention_GBps": attention_bytes(w) / t_a / 1e9,
             "prefetch_GBps": 2 * n_pf * w.bb / t_p / 1e9 if t_p > 0 else None,
             "tokens_per_s_extrapolated": tok_s, "attention_passes": reps}
-        for cfg, key in ((synth.TINY, "tiny_full"), (synth.L70B_TP8, "llama-70b-tp8-share_layer")):
+        others = [(c, k) for c, k in ((synth.TINY, "tiny_full"),
+                                      (synth.LLAMA8B, "llama3-8b-kv_layer"),
+                                      (synth.L70B_TP8, "llama-70b-tp8-share_layer"))
+                  if c.name != w.cfg.name]
+        for cfg, key in others:
             v = Workload(cfg, layers=1, fill="device", staging_slots=1)
             try:
                 ta, tp, n, reps = _oracle_layer(v, 0, per if cfg is not synth.TINY else 0.5)
@@ -277,10 +281,10 @@ def cpu_baseline(w, seconds):
         res["stress_copy_4GiB"] = {"blocks": n_blk, "seconds": t_c,
                                    "GBps": 2 * n_blk * bb / t_c / 1e9}
     res["sample"] = (
-        "one thread: tiny config in full; 8B-shaped layer 0 (all "
-        f"{w.B} sequences, float64 attention, {res['llama3-8b-kv_layer']['attention_passes']} "
-        f"passes) plus its prefetch of {n_pf} blocks, extrapolated to {w.L} layers; 70B-share "
-        f"layer 0 (128 sequences); 4 GiB of single-block copies ({n_blk} x 64 KiB)")
+        f"one thread: {w.cfg.name} layer 0 (all {w.B} sequences, float64 attention, "
+        f"{reps} passes) plus its prefetch of {n_pf} blocks, extrapolated to {w.L} layers; "
+        "layer 0 of the other full-size shape; the tiny config in full; 4 GiB of single-block "
+        f"copies ({n_blk} x 64 KiB)")
     return res
 
 
