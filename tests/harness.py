@@ -48,6 +48,17 @@ def rel_err(out, ref):
     return float((num / den).max()) if num.size else 0.0
 
 
+def elem_err(out, ref, floor=1e-3):
+    """max over elements of |o - ref| / max(|ref|, floor * row max |ref|): the
+    elementwise error with a floor, reported beside the normwise gate."""
+    out = np.asarray(out, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    rowmax = np.abs(ref).max(axis=-1, keepdims=True)
+    den = np.maximum(np.abs(ref), floor * rowmax)
+    den = np.where(den > 0, den, 1.0)
+    return float((np.abs(out - ref) / den).max()) if out.size else 0.0
+
+
 def read_blocks(view, ids):
     """Host copies of the given blocks of a pool view (id -> bytes)."""
     ids = np.unique(np.asarray(ids, dtype=np.int64))

@@ -10,7 +10,7 @@ import torch
 
 import oracle
 import synth
-from harness import Workload, oracle_mirror, read_blocks, rel_err
+from harness import Workload, elem_err, oracle_mirror, read_blocks, rel_err
 
 pytestmark = pytest.mark.gpu
 TOL = 2e-3
@@ -96,6 +96,13 @@ def test_attention_shapes_and_ragged_lengths(ema, impl, hq, hkv, bs, dtype):
         ref = oracle_attention(w, st, 0)
         assert np.all(got[0] == 0.0)                    # empty sequence
         assert rel_err(got, ref) <= TOL, rel_err(got, ref)
+        # elementwise with a floor of 1e-3 of the row's max: the probabilities
+        # keep 16 significant bits, so an element's error stays below 2^-16
+        # of the row max, i.e. 2^-16 / 1e-3 at the floor
+        e = elem_err(got, ref)
+        print(f"  normwise {rel_err(got, ref):.2e}, elementwise (floor 1e-3 of the row max) "
+              f"{e:.2e}", flush=True)
+        assert e <= 2.0 ** -16 / 1e-3, e
     finally:
         w.close()
 
